@@ -1,0 +1,403 @@
+/*
+ * Test infrastructure, not product code: a plain CPU oracle for the batched
+ * backoff n-gram query and the greedy shallow-fusion step.  Only the tests,
+ * the smoke check and the CPU-baseline leg of the benchmark load it.  It shares
+ * no code, header or table with the GPU library.
+ *
+ * What it computes, from the definitions and not from any trie layout:
+ *
+ *   score(c, v)  ARPA backoff rule (Section 2.1): if the n-gram c+(v) is listed,
+ *                its weight W(c v); otherwise B(c) + score(c[1:], v), with
+ *                B(c) = 0 for a context that is not listed, and the <unk>
+ *                weight when even the unigram (v) is missing.  Two results
+ *                are returned: the sum in double (the value of the definition
+ *                for the fp32 inputs), and the fp32 sum taken in the order of
+ *                the paper's Algorithm 1 (an accumulator that starts at 0 and
+ *                adds each backoff weight from the query state downward, and
+ *                one final add of the found weight).  Rounding decisions
+ *                (argmax) use the fp32 value.
+ *   next(c, v)   the state of the longest suffix of c+(v) that is a state
+ *                (Section 2.1, graph representation: states are contexts,
+ *                i.e. listed n-grams of order < N plus the empty context;
+ *                highest-order arcs lead to the (N-1)-suffix state).
+ *   state ids    0 is the empty context; the others are numbered by
+ *                (order, token tuple in lexicographic order).  This is the
+ *                order of arcs sorted by (from_state, token) in Section 2.2.
+ *   greedy step  Section 2.3: plain fusion takes argmax_v of
+ *                fmaf(lambda, lm(v), asr(v)); CTC first takes the plain ASR
+ *                argmax over V+1 classes (blank = V) and keeps blank or the
+ *                previous label unchanged without rescoring, otherwise it
+ *                takes the fused argmax over the other tokens (not blank, not
+ *                the previous label) and advances; the transducer mode keeps
+ *                blank, otherwise takes the fused argmax over all V tokens.
+ *                Ties go to the lowest index (strict '>' scan).
+ *
+ * Parity pins (no external implementation exists): hand-derived values on the
+ * Figure 1 sentence, brute-force history recursion on tiny models, per-context
+ * normalisation of generated models, and the N=1 / N=2 / lambda=0 reductions.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fused multiply-add
+ * is formed anywhere except the explicit fmaf of the fusion rule).
+ */
+#define _GNU_SOURCE
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_MAX_ORDER 10
+
+enum {
+    OR_OK = 0,
+    OR_BAD_ARG = -1,
+    OR_TOKEN = -2,
+    OR_ORDER = -3,
+    OR_DUP = -4,
+    OR_NO_UNK = -7,
+    OR_NOMEM = -20,
+    OR_BAD_STATE = -12,
+};
+
+typedef struct {
+    int32_t V, N;
+    int64_t M;
+    int32_t *ord;   /* [M] */
+    int32_t *tok;   /* [M*N], row i uses its first ord[i] tokens */
+    float *W, *B;   /* [M] */
+    float unk;
+    int has_unk;
+    int64_t cap;    /* hash capacity (power of two) */
+    int64_t *slot;  /* row index or -1 */
+    int64_t S;
+    int64_t *state_row; /* [S], state_row[0] = -1 (empty context) */
+    int64_t *row_state; /* [M], -1 for highest-order n-grams */
+} oracle_model;
+
+static char g_err[256];
+static const char *set_err(const char *msg) {
+    snprintf(g_err, sizeof g_err, "%s", msg);
+    return g_err;
+}
+const char *oracle_last_error(void) { return g_err; }
+
+static uint64_t hash_tuple(const int32_t *t, int k) {
+    uint64_t h = 1469598103934665603ull ^ (uint64_t)k;
+    for (int i = 0; i < k; ++i) {
+        h ^= (uint64_t)(uint32_t)t[i];
+        h *= 1099511628211ull;
+        h ^= h >> 29;
+    }
+    return h;
+}
+
+static int same_tuple(const oracle_model *m, int64_t row, const int32_t *t, int k) {
+    if (m->ord[row] != k) return 0;
+    return memcmp(m->tok + row * m->N, t, (size_t)k * sizeof(int32_t)) == 0;
+}
+
+/* Row of the listed n-gram t[0..k-1], or -1. */
+static int64_t lookup(const oracle_model *m, const int32_t *t, int k) {
+    uint64_t mask = (uint64_t)m->cap - 1;
+    uint64_t i = hash_tuple(t, k) & mask;
+    for (;;) {
+        int64_t r = m->slot[i];
+        if (r < 0) return -1;
+        if (same_tuple(m, r, t, k)) return r;
+        i = (i + 1) & mask;
+    }
+}
+
+static int cmp_state(const void *a, const void *b, void *ctx) {
+    const oracle_model *m = (const oracle_model *)ctx;
+    int64_t ra = *(const int64_t *)a, rb = *(const int64_t *)b;
+    if (m->ord[ra] != m->ord[rb]) return m->ord[ra] < m->ord[rb] ? -1 : 1;
+    const int32_t *ta = m->tok + ra * m->N, *tb = m->tok + rb * m->N;
+    for (int i = 0; i < m->ord[ra]; ++i)
+        if (ta[i] != tb[i]) return ta[i] < tb[i] ? -1 : 1;
+    return 0;
+}
+
+void oracle_free(oracle_model *m) {
+    if (!m) return;
+    free(m->ord); free(m->tok); free(m->W); free(m->B);
+    free(m->slot); free(m->state_row); free(m->row_state);
+    free(m);
+}
+
+int oracle_create(int32_t V, int32_t N, int64_t M, const int32_t *order, const int32_t *tokens,
+                  const float *logprob, const float *backoff, float unk_logprob,
+                  oracle_model **out) {
+    *out = NULL;
+    if (V <= 0 || N < 1 || N > ORACLE_MAX_ORDER || M < 0) { set_err("bad sizes"); return OR_BAD_ARG; }
+    oracle_model *m = (oracle_model *)calloc(1, sizeof *m);
+    if (!m) return OR_NOMEM;
+    m->V = V; m->N = N; m->M = M;
+    m->unk = unk_logprob;
+    m->has_unk = !isnan(unk_logprob);
+    m->ord = (int32_t *)malloc(sizeof(int32_t) * (size_t)(M ? M : 1));
+    m->tok = (int32_t *)malloc(sizeof(int32_t) * (size_t)(M ? M : 1) * (size_t)N);
+    m->W = (float *)malloc(sizeof(float) * (size_t)(M ? M : 1));
+    m->B = (float *)malloc(sizeof(float) * (size_t)(M ? M : 1));
+    m->cap = 16;
+    while (m->cap < 2 * M + 16) m->cap <<= 1;
+    m->slot = (int64_t *)malloc(sizeof(int64_t) * (size_t)m->cap);
+    m->row_state = (int64_t *)malloc(sizeof(int64_t) * (size_t)(M ? M : 1));
+    if (!m->ord || !m->tok || !m->W || !m->B || !m->slot || !m->row_state) {
+        oracle_free(m); set_err("out of memory"); return OR_NOMEM;
+    }
+    memcpy(m->ord, order, sizeof(int32_t) * (size_t)M);
+    memcpy(m->tok, tokens, sizeof(int32_t) * (size_t)M * (size_t)N);
+    memcpy(m->W, logprob, sizeof(float) * (size_t)M);
+    memcpy(m->B, backoff, sizeof(float) * (size_t)M);
+    memset(m->slot, 0xff, sizeof(int64_t) * (size_t)m->cap);
+
+    int64_t n_states = 1;
+    for (int64_t r = 0; r < M; ++r) {
+        int k = m->ord[r];
+        if (k < 1 || k > N) { oracle_free(m); set_err("order out of range"); return OR_ORDER; }
+        const int32_t *t = m->tok + r * N;
+        for (int i = 0; i < k; ++i)
+            if (t[i] < 0 || t[i] >= V) { oracle_free(m); set_err("token out of range"); return OR_TOKEN; }
+        uint64_t mask = (uint64_t)m->cap - 1, i = hash_tuple(t, k) & mask;
+        while (m->slot[i] >= 0) {
+            if (same_tuple(m, m->slot[i], t, k)) { oracle_free(m); set_err("duplicate n-gram"); return OR_DUP; }
+            i = (i + 1) & mask;
+        }
+        m->slot[i] = r;
+        if (k < N) ++n_states;
+    }
+    if (!m->has_unk) {
+        for (int32_t v = 0; v < V; ++v)
+            if (lookup(m, &v, 1) < 0) { oracle_free(m); set_err("missing unigram and no <unk>"); return OR_NO_UNK; }
+    }
+    /* canonical state numbering: empty context, then (order, tuple) ascending */
+    m->S = n_states;
+    m->state_row = (int64_t *)malloc(sizeof(int64_t) * (size_t)n_states);
+    if (!m->state_row) { oracle_free(m); return OR_NOMEM; }
+    m->state_row[0] = -1;
+    int64_t j = 1;
+    for (int64_t r = 0; r < M; ++r)
+        if (m->ord[r] < N) m->state_row[j++] = r;
+    qsort_r(m->state_row + 1, (size_t)(n_states - 1), sizeof(int64_t), cmp_state, m);
+    for (int64_t r = 0; r < M; ++r) m->row_state[r] = -1;
+    for (int64_t s = 1; s < n_states; ++s) m->row_state[m->state_row[s]] = s;
+    *out = m;
+    return OR_OK;
+}
+
+int64_t oracle_num_states(const oracle_model *m) { return m->S; }
+
+/* Context tuple of state s into out[0..N-2]; returns its length, or -1. */
+int oracle_state_context(const oracle_model *m, int64_t s, int32_t *out) {
+    if (s < 0 || s >= m->S) return -1;
+    if (s == 0) return 0;
+    int64_t r = m->state_row[s];
+    memcpy(out, m->tok + r * m->N, sizeof(int32_t) * (size_t)m->ord[r]);
+    return m->ord[r];
+}
+
+/* State id of a context tuple, or -1 if the tuple is not a state. */
+int64_t oracle_state_of(const oracle_model *m, const int32_t *ctx, int k) {
+    if (k == 0) return 0;
+    if (k < 0 || k >= m->N) return -1;
+    int64_t r = lookup(m, ctx, k);
+    return r < 0 ? -1 : m->row_state[r];
+}
+
+/* Longest suffix of g[0..len-1] (at most N-1 tokens) that is a state. */
+static int64_t longest_state_suffix(const oracle_model *m, const int32_t *g, int len) {
+    int jmax = len < m->N - 1 ? len : m->N - 1;
+    for (int j = jmax; j >= 1; --j) {
+        int64_t r = lookup(m, g + (len - j), j);
+        if (r >= 0 && m->row_state[r] >= 0) return m->row_state[r];
+    }
+    return 0;
+}
+
+/* The backoff rule for context c[0..n-1] and token v. */
+static void score_one(const oracle_model *m, const int32_t *c, int n, int32_t v,
+                      float *s32, double *s64, int32_t *next) {
+    int32_t g[ORACLE_MAX_ORDER + 1];
+    float acc32 = 0.0f;
+    double acc64 = 0.0;
+    for (int k = n; k >= 0; --k) {
+        /* g = last k tokens of the context, then v */
+        memcpy(g, c + (n - k), sizeof(int32_t) * (size_t)k);
+        g[k] = v;
+        int64_t r = lookup(m, g, k + 1);
+        if (r >= 0) {
+            *s32 = acc32 + m->W[r];
+            *s64 = acc64 + (double)m->W[r];
+            *next = (int32_t)longest_state_suffix(m, g, k + 1);
+            return;
+        }
+        if (k > 0) {
+            int64_t rc = lookup(m, c + (n - k), k);
+            float b = rc >= 0 ? m->B[rc] : 0.0f;
+            acc32 = acc32 + b;
+            acc64 = acc64 + (double)b;
+        }
+    }
+    *s32 = acc32 + m->unk;
+    *s64 = acc64 + (double)m->unk;
+    *next = 0;
+}
+
+/* Full row for state s: scores and next states of all V tokens. */
+static int score_row(const oracle_model *m, int64_t s, float *s32, double *s64, int32_t *next) {
+    int32_t c[ORACLE_MAX_ORDER];
+    int n = oracle_state_context(m, s, c);
+    if (n < 0) return OR_BAD_STATE;
+    double d;
+    for (int32_t v = 0; v < m->V; ++v)
+        score_one(m, c, n, v, &s32[v], s64 ? &s64[v] : &d, &next[v]);
+    return OR_OK;
+}
+
+typedef struct {
+    const oracle_model *m;
+    const int32_t *states;
+    int64_t b0, b1;
+    float *s32;
+    double *s64;
+    int32_t *next;
+    int rc;
+} adv_job;
+
+static void *adv_worker(void *p) {
+    adv_job *j = (adv_job *)p;
+    int64_t V = j->m->V;
+    for (int64_t b = j->b0; b < j->b1; ++b) {
+        int rc = score_row(j->m, j->states[b], j->s32 + b * V, j->s64 ? j->s64 + b * V : NULL,
+                           j->next + b * V);
+        if (rc) j->rc = rc;
+    }
+    return NULL;
+}
+
+static void run_jobs(void *(*fn)(void *), void *jobs, size_t job_size, int nthreads) {
+    pthread_t th[256];
+    int started = 1;
+    for (; started < nthreads; ++started)
+        if (pthread_create(&th[started], NULL, fn, (char *)jobs + job_size * (size_t)started) != 0) break;
+    for (int t = started; t < nthreads; ++t) fn((char *)jobs + job_size * (size_t)t); /* no thread left */
+    fn(jobs);
+    for (int t = 1; t < started; ++t) pthread_join(th[t], NULL);
+}
+
+static int clamp_threads(int nthreads, int64_t work) {
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > 256) nthreads = 256;
+    if (work < nthreads) nthreads = work > 0 ? (int)work : 1;
+    return nthreads;
+}
+
+/* scores32/next: [B, V]; scores64 may be NULL. */
+int oracle_advance(const oracle_model *m, const int32_t *states, int64_t B, float *scores32,
+                   double *scores64, int32_t *next, int nthreads) {
+    nthreads = clamp_threads(nthreads, B);
+    adv_job jobs[256];
+    for (int t = 0; t < nthreads; ++t) {
+        jobs[t].m = m; jobs[t].states = states;
+        jobs[t].b0 = B * t / nthreads; jobs[t].b1 = B * (t + 1) / nthreads;
+        jobs[t].s32 = scores32; jobs[t].s64 = scores64; jobs[t].next = next; jobs[t].rc = 0;
+    }
+    run_jobs(adv_worker, jobs, sizeof(adv_job), nthreads);
+    for (int t = 0; t < nthreads; ++t) if (jobs[t].rc) return jobs[t].rc;
+    return OR_OK;
+}
+
+enum { MODE_PLAIN = 0, MODE_CTC = 1, MODE_TRANSDUCER = 2 };
+
+/* One greedy step for one hypothesis.  asr has V+1 entries for CTC/transducer
+ * (blank = V) and at least V for plain fusion.  Returns the label. */
+static int32_t greedy_one(const oracle_model *m, const float *asr, int mode, float lambda,
+                          int32_t *state, int32_t *prev, float *lm, int32_t *nx) {
+    int32_t V = m->V;
+    if (mode == MODE_CTC || mode == MODE_TRANSDUCER) {
+        int32_t a = 0;
+        for (int32_t v = 1; v <= V; ++v)
+            if (asr[v] > asr[a]) a = v;
+        if (a == V || (mode == MODE_CTC && a == *prev)) {
+            if (mode == MODE_CTC) *prev = a;
+            return a;
+        }
+    }
+    score_row(m, *state, lm, NULL, nx);
+    int32_t best = -1;
+    float bestval = 0.0f;
+    for (int32_t v = 0; v < V; ++v) {
+        if (mode == MODE_CTC && v == *prev) continue;
+        float f = fmaf(lambda, lm[v], asr[v]);
+        if (best < 0 || f > bestval) { best = v; bestval = f; }
+    }
+    *state = nx[best];
+    if (mode == MODE_CTC) *prev = best;
+    return best;
+}
+
+/* One fused step over B hypotheses (in-place states/prev). */
+int oracle_greedy_step(const oracle_model *m, const float *asr, int64_t B, int64_t ld, int mode,
+                       float lambda, int32_t *states, int32_t *prev, int32_t *tokens_out) {
+    if (mode < 0 || mode > 2) return OR_BAD_ARG;
+    float *lm = (float *)malloc(sizeof(float) * (size_t)m->V);
+    int32_t *nx = (int32_t *)malloc(sizeof(int32_t) * (size_t)m->V);
+    if (!lm || !nx) { free(lm); free(nx); return OR_NOMEM; }
+    int rc = OR_OK;
+    for (int64_t b = 0; b < B; ++b) {
+        if (states[b] < 0 || states[b] >= m->S) { rc = OR_BAD_STATE; break; }
+        int32_t p = prev ? prev[b] : 0;
+        tokens_out[b] = greedy_one(m, asr + b * ld, mode, lambda, &states[b], &p, lm, nx);
+        if (prev) prev[b] = p;
+    }
+    free(lm); free(nx);
+    return rc;
+}
+
+typedef struct {
+    const oracle_model *m;
+    const float *asr;
+    int64_t T, ld, b0, b1;
+    int mode;
+    float lambda;
+    int32_t start;
+    int32_t *labels, *states_out;
+    int rc;
+} dec_job;
+
+static void *dec_worker(void *p) {
+    dec_job *j = (dec_job *)p;
+    const oracle_model *m = j->m;
+    float *lm = (float *)malloc(sizeof(float) * (size_t)m->V);
+    int32_t *nx = (int32_t *)malloc(sizeof(int32_t) * (size_t)m->V);
+    if (!lm || !nx) { free(lm); free(nx); j->rc = OR_NOMEM; return NULL; }
+    for (int64_t b = j->b0; b < j->b1; ++b) {
+        int32_t s = j->start, prev = m->V;
+        for (int64_t t = 0; t < j->T; ++t) {
+            const float *row = j->asr + (b * j->T + t) * j->ld;
+            j->labels[b * j->T + t] = greedy_one(m, row, j->mode, j->lambda, &s, &prev, lm, nx);
+            j->states_out[b * j->T + t] = s;
+        }
+    }
+    free(lm); free(nx);
+    return NULL;
+}
+
+/* Whole greedy decode: asr [B, T, ld]; labels and states after each frame [B, T].
+ * Starts at state `start` with previous label = blank (V). */
+int oracle_decode(const oracle_model *m, const float *asr, int64_t B, int64_t T, int64_t ld, int mode,
+                  float lambda, int32_t start, int32_t *labels, int32_t *states_out, int nthreads) {
+    if (mode < 0 || mode > 2 || start < 0 || start >= m->S) return OR_BAD_ARG;
+    nthreads = clamp_threads(nthreads, B);
+    dec_job jobs[256];
+    for (int t = 0; t < nthreads; ++t) {
+        dec_job d = {m, asr, T, ld, B * t / nthreads, B * (t + 1) / nthreads, mode, lambda, start,
+                     labels, states_out, 0};
+        jobs[t] = d;
+    }
+    run_jobs(dec_worker, jobs, sizeof(dec_job), nthreads);
+    for (int t = 0; t < nthreads; ++t) if (jobs[t].rc) return jobs[t].rc;
+    return OR_OK;
+}

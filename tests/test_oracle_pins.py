@@ -1,0 +1,399 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+No implementation of the method exists to compare with, so the oracle is tied
+down by: hand-derived values on the Figure 1 sentence (tests/golden), the
+backoff rule restated on raw histories (brute force on tiny models), per-context
+normalisation of models built normalised, the textbook reductions (unigram
+model, bigram backoff, lambda = 0 fusion, greedy CTC), structural invariants of
+the suffix graph, and the fp32 summation error bound.  The last test plants
+mistakes in copies of the oracle and checks that some pin catches each one.
+"""
+
+import itertools
+import json
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle
+from oracle.bruteforce import BruteForce
+from synth import (asr_logprobs, generate_model, make_config_model, state_ids_of, tiny_model,
+                   uniform_states)
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GOLDEN = os.path.join(HERE, "golden")
+
+
+def fig1_list():
+    with open(os.path.join(GOLDEN, "fig1_trigram.json")) as f:
+        fx = json.load(f)
+    N = fx["max_order"]
+    ng = fx["ngrams"]
+    order = np.array([len(g[0]) for g in ng], np.int32)
+    tokens = np.full((len(ng), N), -1, np.int32)
+    for i, g in enumerate(ng):
+        tokens[i, :len(g[0])] = g[0]
+    W = np.array([g[1] for g in ng], np.float32)
+    B = np.array([g[2] for g in ng], np.float32)
+    return fx, (len(fx["vocab"]), N, order, tokens, W, B)
+
+
+# ---------------------------------------------------------------- pin checks
+# Each takes the oracle library path so that the planted-mistake test can run
+# the same checks against a mutated oracle.
+
+def check_worked_example(lib_path):
+    fx, lst = fig1_list()
+    o = Oracle(*lst, lib_path=lib_path)
+    assert o.num_states == len(fx["state_contexts"])
+    for s, ctx in enumerate(fx["state_contexts"]):
+        assert o.state_context(s) == tuple(ctx)
+    for s, row in fx["rows"].items():
+        s32, nx, s64 = o.advance(np.array([int(s)], np.int32), want64=True)
+        np.testing.assert_allclose(s64[0], row["scores"], atol=1e-6)
+        np.testing.assert_allclose(s32[0], row["scores"], atol=1e-6)
+        assert nx[0].tolist() == row["next"]
+    st, tot = 0, 0.0
+    sent = fx["sentence"]
+    for tok, exp_state, exp_score in zip(sent["tokens"], sent["states"], sent["scores"]):
+        s32, nx, s64 = o.advance(np.array([st], np.int32), want64=True)
+        assert abs(s64[0, tok] - exp_score) < 1e-6
+        tot += s64[0, tok]
+        st = int(nx[0, tok])
+        assert st == exp_state
+    assert abs(tot - sent["total"]) < 1e-5
+
+
+def check_bruteforce_tiny(lib_path, seeds=(0, 1, 2, 3), max_hist_extra=1):
+    for seed in seeds:
+        V = 4 + seed % 3
+        N = 2 + seed % 3
+        model = tiny_model(V, N, seed=100 + seed, fill=0.5)
+        o = Oracle.from_model(model, lib_path=lib_path, shuffle_seed=seed)
+        bf = BruteForce.from_model(model)
+        S = o.num_states
+        rows = o.advance(np.arange(S, dtype=np.int32), want64=True)
+        s32, nx, s64 = rows
+        ctx_of = [o.state_context(s) for s in range(S)]
+        for L in range(0, N + max_hist_extra):
+            for h in itertools.product(range(V), repeat=L):
+                # feed the history from the empty context through the oracle's next states
+                st = 0
+                for t in h:
+                    st = int(nx[st, t])
+                assert ctx_of[st] == bf.state_context(h), (seed, h)
+                for v in range(V):
+                    assert abs(s64[st, v] - bf.score(h, v)) < 1e-9, (seed, h, v)
+                    assert ctx_of[int(nx[st, v])] == bf.state_context(h + (v,)), (seed, h, v)
+
+
+def check_normalisation(lib_path, model, states, tol=1e-5):
+    o = Oracle.from_model(model, lib_path=lib_path)
+    s32, nx, s64 = o.advance(states, nthreads=8, want64=True)
+    tot = np.exp(s64).sum(axis=1)
+    assert np.abs(tot - 1.0).max() < tol, np.abs(tot - 1.0).max()
+    tot32 = np.exp(s32.astype(np.float64)).sum(axis=1)
+    assert np.abs(tot32 - 1.0).max() < tol
+
+
+def check_lambda_zero_and_ties(lib_path):
+    model = tiny_model(7, 3, seed=11)
+    o = Oracle.from_model(model, lib_path=lib_path)
+    rng = np.random.default_rng(5)
+    S = o.num_states
+    states = rng.integers(0, S, 64).astype(np.int32)
+    asr = rng.standard_normal((64, 7)).astype(np.float32)
+    asr[:8] = 0.25                                       # full ties: lowest index wins
+    asr[8:16, 2] = asr[8:16, 5] = 9.0                     # two-way ties
+    st = states.copy()
+    tok = o.greedy_step(asr, MODE_PLAIN, 0.0, st)
+    exp = np.argmax(asr, axis=1)                         # numpy: first maximal index
+    assert tok.tolist() == exp.tolist()
+    _, nx, _ = o.advance(states)
+    assert st.tolist() == nx[np.arange(64), exp].tolist()
+
+
+def check_ctc_rules(lib_path):
+    fx, lst = fig1_list()
+    o = Oracle(*lst, lib_path=lib_path)
+    V = 5
+    lam = 10.0
+    # frame 0: raw ASR prefers 'cat' (1) a little, LM from the root prefers 'the' (0)
+    f0 = np.array([-1.2, -1.0, -3.0, -3.0, -3.0, -4.0], np.float32)
+    # frame 1: 'the' wins raw and equals the previous label -> kept, no advance
+    f1 = np.array([-0.1, -3.0, -3.0, -3.0, -3.0, -4.0], np.float32)
+    # frame 2: blank wins raw -> kept, no advance
+    f2 = np.array([-3.0, -3.0, -3.0, -3.0, -3.0, -0.1], np.float32)
+    # frame 3: 'on' wins raw; fused over tokens other than the previous label (blank here)
+    f3 = np.array([-3.0, -3.0, -3.0, -0.5, -3.0, -4.0], np.float32)
+    asr = np.stack([f0, f1, f2, f3])[None]
+    labels, states = o.decode(asr, MODE_CTC, lam)
+    # frame 0 from the root: fused(v) = asr + 10*unigram -> 'the' (-1.2-10) beats 'cat' (-1.0-20)
+    assert labels[0].tolist()[:3] == [0, 0, V]
+    assert states[0].tolist()[:3] == [1, 1, 1]
+    # frame 3 at state 1 'the': fused = asr + 10*lm; lm row [-1.5,-0.7,-2.5,-2.5,-0.9]
+    row = np.array([-1.5, -0.7, -2.5, -2.5, -0.9]) * lam + f3[:V]
+    assert labels[0, 3] == int(np.argmax(row)) == 1
+    assert states[0, 3] == 6
+    # the repeat rule excludes the previous label from stage 2: previous 'cat'
+    st = np.array([6], np.int32)
+    prev = np.array([1], np.int32)
+    f = np.array([[-3.0, -0.9, -0.5, -3.0, -3.0, -4.0]], np.float32)   # 'sat' raw winner
+    f[0, 1] = -0.6                                                      # repeat close behind
+    tok = o.greedy_step(f, MODE_CTC, lam, st, prev)
+    assert tok[0] == 2 and st[0] == 8 and prev[0] == 2
+    # transducer: blank kept, otherwise fused argmax over all V
+    st = np.array([0], np.int32)
+    tok = o.greedy_step(np.array([[-3, -3, -3, -3, -3, -0.1]], np.float32), MODE_TRANSDUCER, lam, st)
+    assert tok[0] == V and st[0] == 0
+    tok = o.greedy_step(np.array([[-1.2, -1.0, -3, -3, -3, -4]], np.float32), MODE_TRANSDUCER, lam, st)
+    assert tok[0] == 0 and st[0] == 1
+
+
+def check_generator_ids(lib_path):
+    model = make_config_model(1)
+    o = Oracle.from_model(model, lib_path=lib_path, shuffle_seed=3)
+    N = model.max_order
+    for k in range(1, N):
+        toks = model.level_tokens(k)
+        ids = state_ids_of(model, toks)
+        for i in range(0, len(toks), max(1, len(toks) // 50)):
+            assert o.state_of(toks[i]) == ids[i]
+            assert o.state_context(int(ids[i])) == tuple(int(t) for t in toks[i])
+
+
+# ---------------------------------------------------------------- the tests
+
+def test_worked_example_fig1(oracle_lib):
+    check_worked_example(oracle.LIB_PATH)
+
+
+def test_bruteforce_history_recursion_tiny(oracle_lib):
+    check_bruteforce_tiny(oracle.LIB_PATH, seeds=range(6))
+
+
+def test_bruteforce_config1_sampled_histories(oracle_lib):
+    model = make_config_model(1)
+    o = Oracle.from_model(model)
+    bf = BruteForce.from_model(model)
+    rng = np.random.default_rng(7)
+    S = o.num_states
+    s32, nx, s64 = o.advance(np.arange(S, dtype=np.int32), want64=True)
+    for _ in range(3000):
+        L = int(rng.integers(0, 6))
+        # histories biased toward listed n-grams so deep states are exercised
+        h = []
+        st = 0
+        for _ in range(L):
+            v = int(np.argmax(s64[st] + rng.gumbel(size=model.vocab_size)))
+            h.append(v)
+            st = int(nx[st, v])
+        assert o.state_context(st) == bf.state_context(h)
+        v = int(rng.integers(0, model.vocab_size))
+        assert abs(s64[st, v] - bf.score(h, v)) < 1e-9
+
+
+def test_normalisation_config1_all_states(oracle_lib):
+    model = make_config_model(1)
+    check_normalisation(oracle.LIB_PATH, model, np.arange(model.num_states, dtype=np.int32))
+
+
+def test_normalisation_config2_sampled(oracle_lib):
+    model = make_config_model(2)
+    check_normalisation(oracle.LIB_PATH, model, uniform_states(model, 3000, seed=9))
+
+
+def test_normalisation_tiny_with_unk(oracle_lib):
+    model = tiny_model(9, 3, seed=21, n_unigrams=6)
+    assert not np.isnan(model.unk_logprob)
+    check_normalisation(oracle.LIB_PATH, model, np.arange(model.num_states, dtype=np.int32))
+
+
+def test_unigram_model_rows_equal_unigram_row(oracle_lib):
+    model = generate_model(50, [50], 1.1, seed=3)
+    o = Oracle.from_model(model)
+    assert o.num_states == 1
+    s32, nx, _ = o.advance(np.zeros(3, np.int32))
+    order, tokens, W, B = model.to_list()
+    exp = np.empty(50, np.float32)
+    exp[tokens[:, 0]] = W
+    assert (s32 == exp).all() and (nx == 0).all()
+
+
+def test_bigram_textbook_backoff(oracle_lib):
+    model = generate_model(30, [30, 300], 1.0, seed=4)
+    o = Oracle.from_model(model)
+    order, tokens, W, B = model.to_list()
+    Wd = {tuple(t[:k]): w for k, t, w in zip(order, tokens, W)}
+    Bd = {tuple(t[:k]): b for k, t, b in zip(order, tokens, B)}
+    s32, nx, s64 = o.advance(np.arange(o.num_states, dtype=np.int32), want64=True)
+    for u in range(30):
+        su = o.state_of([u])
+        assert su == u + 1
+        for v in range(30):
+            if (u, v) in Wd:
+                exp, exp_next = float(Wd[(u, v)]), v + 1
+            else:
+                exp, exp_next = float(Bd[(u,)]) + float(Wd[(v,)]), v + 1
+            assert abs(s64[su, v] - exp) < 1e-12
+            assert nx[su, v] == exp_next
+
+
+def test_full_coverage_context_needs_no_backoff(oracle_lib):
+    # every bigram of token 0 is listed: that context's row is its own weights
+    V = 12
+    model = generate_model(V, [V, 5 * V], 1.0, seed=8)
+    order, tokens, W, B = model.to_list()
+    full = np.array([[0, v] for v in range(V)], np.int32)
+    keep = ~((order == 2) & (tokens[:, 0] == 0))
+    tok2 = np.concatenate([tokens[keep], np.pad(full, ((0, 0), (0, 0)), constant_values=-1)])
+    w_full = np.log(np.full(V, 1.0 / V)).astype(np.float32)
+    o = Oracle(V, 2, np.concatenate([order[keep], np.full(V, 2, np.int32)]), tok2,
+               np.concatenate([W[keep], w_full]), np.concatenate([B[keep], np.zeros(V, np.float32)]))
+    s32, nx, _ = o.advance(np.array([o.state_of([0])], np.int32))
+    assert (s32[0] == w_full).all()
+    # and a context missing exactly one continuation backs off for that token only
+    miss = 7
+    sel = np.ones(len(o_list := tok2), bool)
+    sel[len(tokens[keep]) + miss] = False
+    o2 = Oracle(V, 2, np.concatenate([order[keep], np.full(V, 2, np.int32)])[sel], tok2[sel],
+                np.concatenate([W[keep], w_full])[sel],
+                np.concatenate([B[keep], np.zeros(V, np.float32)])[sel])
+    s32b, _, _ = o2.advance(np.array([o2.state_of([0])], np.int32))
+    bo = float(B[(order == 1) & (tokens[:, 0] == 0)][0])
+    w1 = float(W[(order == 1) & (tokens[:, 0] == miss)][0])
+    assert s32b[0, miss] == np.float32(np.float32(0.0) + np.float32(bo)) + np.float32(w1)
+    assert (np.delete(s32b[0], miss) == np.delete(w_full, miss)).all()
+
+
+def test_structural_invariants_config2(oracle_lib):
+    model = make_config_model(2)
+    o = Oracle.from_model(model)
+    states = uniform_states(model, 200, seed=12)
+    _, nx, _ = o.advance(states, nthreads=8)
+    N = model.max_order
+    for b, s in enumerate(states):
+        c = o.state_context(int(s))
+        for v in range(0, model.vocab_size, 7):
+            n = int(nx[b, v])
+            assert n >= 0
+            cn = o.state_context(n)
+            assert len(cn) <= min(len(c) + 1, N - 1)
+            full = c + (v,)
+            assert full[len(full) - len(cn):] == cn
+
+
+def test_fp32_fold_within_rounding_bound(oracle_lib):
+    model = make_config_model(2)
+    o = Oracle.from_model(model)
+    states = uniform_states(model, 300, seed=13)
+    s32, _, s64 = o.advance(states, nthreads=8, want64=True)
+    # at most N-1 backoff adds plus one weight add, each rounded once (unit 2^-24)
+    N = model.max_order
+    bound = N * 2.0 ** -24 * (np.abs(s64) + 8.0 * N)
+    assert (np.abs(s32 - s64) <= bound).all()
+    assert np.abs(s32 - s64).max() < 1e-5
+
+
+def test_lambda_zero_plain_is_asr_argmax(oracle_lib):
+    check_lambda_zero_and_ties(oracle.LIB_PATH)
+
+
+def test_ctc_rules_hand_cases(oracle_lib):
+    check_ctc_rules(oracle.LIB_PATH)
+
+
+def test_ctc_lambda_zero_is_textbook_greedy_ctc(oracle_lib):
+    model = make_config_model(1)
+    o = Oracle.from_model(model)
+    V = model.vocab_size
+    asr = asr_logprobs((6, 80, V + 1), seed=14, blank_boost=2.0)
+    # force some repeats: copy frame t-1 into frame t here and there
+    asr[:, 1::5] = asr[:, 0::5][:, : asr[:, 1::5].shape[1]]
+    labels, _ = o.decode(asr, MODE_CTC, 0.0)
+    raw = np.argmax(asr, axis=2)
+    assert (labels == raw).all()
+
+    def collapse(row):
+        out, prev = [], V
+        for a in row:
+            if a != V and a != prev:
+                out.append(int(a))
+            prev = a
+        return out
+
+    for b in range(6):
+        # the advancing frames (non-blank, non-repeat) are exactly the collapsed sequence
+        adv = [int(labels[b, t]) for t in range(80)
+               if labels[b, t] != V and labels[b, t] != (labels[b, t - 1] if t else V)]
+        assert adv == collapse(raw[b])
+
+
+def test_generator_and_oracle_number_states_alike(oracle_lib):
+    check_generator_ids(oracle.LIB_PATH)
+
+
+def test_error_codes():
+    fx, (V, N, order, tokens, W, B) = fig1_list()
+    with pytest.raises(oracle.OracleError) as e:
+        Oracle(V, N, np.append(order, 1), np.vstack([tokens, tokens[:1]]), np.append(W, 0), np.append(B, 0))
+    assert e.value.code == -4
+    bad = tokens.copy(); bad[3, 0] = V
+    with pytest.raises(oracle.OracleError) as e:
+        Oracle(V, N, order, bad, W, B)
+    assert e.value.code == -2
+    with pytest.raises(oracle.OracleError) as e:
+        Oracle(V, N, order[1:], tokens[1:], W[1:], B[1:])          # 'the' unigram missing, no <unk>
+    assert e.value.code == -7
+
+
+# ------------------------------------------------- planted mistakes are caught
+
+MUTANTS = {
+    "dropped backoff term": ("float b = rc >= 0 ? m->B[rc] : 0.0f;", "float b = 0.0f; (void)rc;"),
+    "backoff sign": ("float b = rc >= 0 ? m->B[rc] : 0.0f;", "float b = rc >= 0 ? -m->B[rc] : 0.0f;"),
+    "backoff of the prefix": ("int64_t rc = lookup(m, c + (n - k), k);", "int64_t rc = lookup(m, c, k);"),
+    "context prefix instead of suffix": ("memcpy(g, c + (n - k), sizeof(int32_t) * (size_t)k);",
+                                         "memcpy(g, c, sizeof(int32_t) * (size_t)k);"),
+    "next drops the token": ("*next = (int32_t)longest_state_suffix(m, g, k + 1);",
+                             "*next = (int32_t)longest_state_suffix(m, g, k);"),
+    "reversed numbering": ("if (ta[i] != tb[i]) return ta[i] < tb[i] ? -1 : 1;",
+                           "if (ta[i] != tb[i]) return ta[i] > tb[i] ? -1 : 1;"),
+    "transposed fusion operands": ("float f = fmaf(lambda, lm[v], asr[v]);", "float f = fmaf(lambda, asr[v], lm[v]);"),
+    "repeat rescored": ("if (a == V || (mode == MODE_CTC && a == *prev)) {", "if (a == V) {"),
+    "last index wins ties": ("if (best < 0 || f > bestval) { best = v; bestval = f; }",
+                             "if (best < 0 || f >= bestval) { best = v; bestval = f; }"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name, tmp_path):
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = open(oracle.SRC_PATH).read()
+    old, new = MUTANTS[name]
+    assert src.count(old) == 1, f"mutation site for '{name}' not found exactly once"
+    path = tmp_path / "mutant.c"
+    path.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libmutant.so")
+    subprocess.run(["gcc", *oracle.CFLAGS, "-w", "-o", lib, str(path), "-lm"], check=True)
+    small = make_config_model(1)
+    checks = [
+        lambda: check_worked_example(lib),
+        lambda: check_bruteforce_tiny(lib, seeds=(0, 1, 2)),
+        lambda: check_normalisation(lib, small, np.arange(small.num_states, dtype=np.int32)),
+        lambda: check_lambda_zero_and_ties(lib),
+        lambda: check_ctc_rules(lib),
+        lambda: check_generator_ids(lib),
+    ]
+    caught = 0
+    for chk in checks:
+        try:
+            chk()
+        except (AssertionError, oracle.OracleError):
+            caught += 1
+    assert caught >= 1, f"no pin caught the planted mistake '{name}'"

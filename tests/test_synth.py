@@ -1,0 +1,92 @@
+"""The seeded generators: closure, counts, determinism and the normalising construction."""
+
+import numpy as np
+
+from synth import (CONFIGS, asr_logprobs, generate_model, lookup_ids, make_config_model,
+                   phrase_states, tiny_model, uniform_states)
+
+
+def _closure_ok(model):
+    for k in range(2, model.max_order + 1):
+        t = model.level_tokens(k)
+        assert (lookup_ids(model, t[:, :-1]) >= 0).all(), f"prefix closure at order {k}"
+        assert (lookup_ids(model, t[:, 1:]) >= 0).all(), f"suffix closure at order {k}"
+        # lexicographic order, no duplicates
+        key = np.lexsort(t.T[::-1])
+        assert (key == np.arange(len(t))).all()
+        assert (np.diff(model.levels[k].pid * model.vocab_size + model.levels[k].tok) > 0).all()
+
+
+def _construction_identity(model, tol=2e-6):
+    """sum_E P(v|c) + exp(B(c)) * (1 - sum_E P(v|c[1:])) = 1 for every context."""
+    V = model.vocab_size
+    for k in range(2, model.max_order + 1):
+        lv, prev = model.levels[k], model.levels[k - 1]
+        n = len(prev.tok)
+        m = np.bincount(lv.pid, weights=np.exp(lv.W.astype(np.float64)), minlength=n)
+        l = np.bincount(lv.pid, weights=np.exp(prev.W[lv.sid].astype(np.float64)), minlength=n)
+        cnt = np.bincount(lv.pid, minlength=n)
+        tot = m + np.exp(prev.B.astype(np.float64)) * (1.0 - l)
+        sel = cnt < V
+        assert np.abs(tot[sel] - 1.0).max() < tol
+    p1 = np.exp(model.levels[1].W.astype(np.float64)).sum()
+    if not np.isnan(model.unk_logprob):
+        p1 += (V - len(model.levels[1].tok)) * np.exp(np.float64(model.unk_logprob))
+    assert abs(p1 - 1.0) < 1e-6
+
+
+def test_config_counts_and_closure():
+    for i in (1, 2):
+        spec = CONFIGS[i]
+        m = make_config_model(i)
+        assert m.counts == list(spec.counts)
+        assert m.num_states == 1 + sum(spec.counts[:-1])
+        _closure_ok(m)
+        _construction_identity(m)
+
+
+def test_tiny_models_closed_and_normalised():
+    for seed in range(5):
+        m = tiny_model(5 + seed, 2 + seed % 4, seed=seed)
+        _closure_ok(m)
+        _construction_identity(m)
+    m = tiny_model(9, 3, seed=21, n_unigrams=6)
+    _closure_ok(m)
+    _construction_identity(m)
+
+
+def test_deterministic_from_seed():
+    a = generate_model(64, [64, 500, 400], 1.1, seed=5).to_list()
+    b = generate_model(64, [64, 500, 400], 1.1, seed=5).to_list()
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_shuffled_list_is_a_permutation():
+    m = make_config_model(1)
+    o1, t1, w1, b1 = m.to_list()
+    o2, t2, w2, b2 = m.to_list(shuffle_seed=1)
+    k1 = np.lexsort(np.column_stack([t1, o1]).T[::-1])
+    k2 = np.lexsort(np.column_stack([t2, o2]).T[::-1])
+    assert np.array_equal(t1[k1], t2[k2]) and np.array_equal(w1[k1], w2[k2])
+
+
+def test_phrase_model_and_deep_states():
+    # a scaled-down version of the context-biasing recipe
+    phrases = [np.array(p) for p in ([1, 2, 3, 4, 5, 6], [7, 8, 9, 10, 11], [3, 4, 5, 6, 7, 8, 9])]
+    m = generate_model(32, [32, 200, 300, 200, 100, 30], 1.05, seed=2, phrases=phrases)
+    _closure_ok(m)
+    _construction_identity(m)
+    st = phrase_states(m, 16, seed=1)
+    first5 = m.state_offset(5)
+    assert (st >= first5).all() and (st < m.num_states).all()
+
+
+def test_uniform_states_and_asr():
+    m = make_config_model(1)
+    s = uniform_states(m, 1000, seed=3)
+    assert s.dtype == np.int32 and s.min() >= 0 and s.max() < m.num_states
+    a = asr_logprobs((3, 7, 129), seed=1, blank_boost=4.0)
+    assert a.dtype == np.float32 and a.shape == (3, 7, 129)
+    assert np.abs(np.exp(a.astype(np.float64)).sum(-1) - 1).max() < 1e-5
+    assert (np.argmax(a, -1) == 128).mean() > 0.0

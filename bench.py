@@ -1,0 +1,234 @@
+"""Benchmark of the batched backoff query and the fused greedy step on one MI355X.
+
+Workload (the 20M n-gram 6-gram model, V = 1024, synthetic and seeded): a
+step is one ``advance`` launch over 128 independent batches of 512 hypotheses
+(65,536 uniformly drawn states), writing scores [65536, 1024] fp32 and next
+states [65536, 1024] int32 -- 512 MiB, more than the 256 MB Infinity Cache, so
+the output really streams to HBM.  The value is (state, token) scores per
+second over the timed steps.  The same run also reports:
+
+* roofline: algorithmic HBM bytes per launch (library ``query_bytes``: output
+  rows plus the records and arcs of chain states of order >= 2) divided by the
+  mean kernel duration from HIP events on the launch stream, against 8 TB/s;
+  ``traffic`` is the measured HBM bytes per launch from the committed rocprofv3
+  counter summary when it was taken on the current kernel source, else null;
+* latency of a single 512-hypothesis call (median of 100);
+* the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame;
+* cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
+  host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "LM (state,token) scores/s + achieved HBM GB/s for batched advance; fused step/s"
+PEAK_HBM_GBPS = 8000.0
+KERNEL_SOURCES = ["paper_2505_22857_amd/csrc/advance.hip", "paper_2505_22857_amd/csrc/walk.h",
+                  "paper_2505_22857_amd/csrc/trie.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "advance_cfg4_traffic.md")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """Measured HBM bytes per launch from the counter summary, if it matches this kernel."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    txt = open(TRAFFIC_FILE).read()
+    m_hash = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", txt)
+    m_val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m_hash or not m_val or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_val.group(1))
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--batches", type=int, default=128, help="512-hypothesis batches per step")
+    ap.add_argument("--fused-frames", type=int, default=1000)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time; 0 skips")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 512 MiB device copy (for counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
+              "(the query is replicated per GPU with no exchange, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2505_22857_amd as ng
+    from synth import CONFIGS, make_config_model, seed_for, uniform_states
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    spec = CONFIGS[4]
+    t0 = time.time()
+    model = make_config_model(4)
+    log(f"model generated in {time.time() - t0:.1f}s: counts {model.counts}")
+    t0 = time.time()
+    lm = ng.NgpuLM.from_model(model)
+    log(f"trie built in {time.time() - t0:.1f}s: {lm.num_states} states, {lm.num_arcs} arcs, "
+        f"{lm.device_bytes / 2**20:.1f} MiB")
+    lm.upload(dev)
+    V = lm.vocab_size
+    Bb = spec.batch
+    R = args.batches
+    B = R * Bb
+    states_np = uniform_states(model, B, seed=seed_for(4) + 1000)
+    states = torch.from_numpy(states_np).to(dev)
+    scores = torch.empty((B, V), dtype=torch.float32, device=dev)
+    nxt = torch.empty((B, V), dtype=torch.int32, device=dev)
+    hbm_bytes, total_bytes = lm.query_bytes(states_np)
+    stream = torch.cuda.current_stream()
+
+    if args.copy_calibration:
+        src = torch.empty(2**29 // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("copy calibration: 5 copies of 512 MiB")
+        del src, dst
+
+    # ---- single 512-hypothesis call latency
+    s512, n512 = scores[:Bb], nxt[:Bb]
+    for _ in range(10):
+        lm.advance(states[:Bb], s512, n512)
+    torch.cuda.synchronize()
+    lat = []
+    for r in range(100):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        sl = slice((r % R) * Bb, (r % R + 1) * Bb)
+        e0.record(stream)
+        lm.advance(states[sl], scores[sl], nxt[sl])
+        e1.record(stream)
+        lat.append((e0, e1))
+    torch.cuda.synchronize()
+    lat_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in lat]))
+    log(f"single B={Bb} call: median {lat_us:.1f} us")
+
+    # ---- sustained: one launch over all R batches per step
+    for _ in range(args.warmup):
+        lm.advance(states, scores, nxt)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record(stream)
+        lm.advance(states, scores, nxt)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    assert lm.check_states() == 0
+    kern_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    mean_ms = float(kern_ms.mean())
+    ms_per_step = wall * 1e3 / args.steps
+    value = B * V * args.steps / wall
+    achieved = hbm_bytes / (mean_ms * 1e-3) / 1e9
+    log(f"advance B={B}: wall {ms_per_step:.3f} ms/step, kernel mean {mean_ms:.3f} ms "
+        f"(min {kern_ms.min():.3f}), {achieved:.0f} GB/s algorithmic HBM, "
+        f"{total_bytes / (mean_ms * 1e-3) / 1e9:.0f} GB/s incl. cache-resident rows")
+
+    # ---- fused greedy CTC step (the config-5 shape), per frame
+    fspec = CONFIGS[5]
+    Bf, T = fspec.batch, args.fused_frames
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed_for(5))
+    logits = torch.randn((T, Bf, V + 1), generator=g, device=dev, dtype=torch.float32) * 3.0
+    logits[..., V] += fspec.blank_boost
+    asr = torch.log_softmax(logits, dim=-1)
+    del logits
+    fst = torch.zeros(Bf, dtype=torch.int32, device=dev)
+    prev = torch.full((Bf,), V, dtype=torch.int32, device=dev)
+    tok = torch.empty(Bf, dtype=torch.int32, device=dev)
+    for t in range(min(T, 20)):
+        lm.fused_greedy_step(asr[t], fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, tokens=tok)
+    fst.zero_()
+    prev.fill_(V)
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    f0.record(stream)
+    for t in range(T):
+        lm.fused_greedy_step(asr[t], fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, tokens=tok)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    f_ms = f0.elapsed_time(f1)
+    assert lm.check_states() == 0
+    fused = {"workload": f"CTC, B={Bf} utterances x {T} frames, {V + 1} classes, lambda={fspec.lam}, "
+                         "one launch per frame",
+             "steps_per_s": T / (f_ms * 1e-3), "frames_per_s": Bf * T / (f_ms * 1e-3),
+             "us_per_step": f_ms * 1e3 / T}
+    log(f"fused CTC: {fused['us_per_step']:.1f} us/step, {fused['frames_per_s']:.3g} frames/s")
+    del asr
+
+    # ---- CPU oracle on a bounded sample of the same workload
+    cpu = None
+    if args.cpu_seconds > 0:
+        from oracle import Oracle
+        cores = len(os.sched_getaffinity(0))
+        o = Oracle.from_model(model)
+        probe = states_np[:256]
+        t0 = time.perf_counter()
+        o.advance(probe, nthreads=cores)
+        dt = time.perf_counter() - t0
+        n = int(min(B, max(256, args.cpu_seconds / max(dt, 1e-6) * 256)))
+        sample = states_np[:n]
+        t0 = time.perf_counter()
+        o.advance(sample, nthreads=cores)
+        dt = time.perf_counter() - t0
+        cpu = {"value": n * V / dt, "unit": "scores/s", "cores": cores, "kind": "oracle",
+               "sample": f"first {n} of the {B} benchmark states, full {V}-token rows, {dt:.1f}s"}
+        log(f"oracle: {cpu['value']:.3g} scores/s on {cores} cores")
+        del o
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "scores/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"6-gram V={V} 20M n-grams (trie {lm.device_bytes / 2**20:.0f} MiB), "
+                               f"advance over {R} batches of {Bb} uniform states per launch",
+                   "vocab": V, "order": model.max_order, "ngrams": model.num_ngrams,
+                   "states": lm.num_states, "batch": Bb, "batches_per_step": R, "hyps_per_step": B},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": committed_traffic(),
+                     "bytes_per_launch": hbm_bytes, "kernel_ms": mean_ms,
+                     "total_bytes_per_launch": total_bytes,
+                     "total_gbps": total_bytes / (mean_ms * 1e-3) / 1e9},
+        "latency_b512_us": lat_us,
+        "fused": fused,
+        "cpu_baseline": cpu,
+        "kernel_source_sha256": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

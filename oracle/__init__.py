@@ -60,7 +60,7 @@ def load(path: str = LIB_PATH):
                                        ctypes.c_float, vp, vp, vp]
     lib.oracle_greedy_step.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
-                                  ctypes.c_int, ctypes.c_float, ctypes.c_int32, vp, vp, ctypes.c_int]
+                                  ctypes.c_int, ctypes.c_float, vp, vp, vp, ctypes.c_int]
     lib.oracle_decode.restype = ctypes.c_int
     lib.oracle_last_error.restype = ctypes.c_char_p
     _lib_cache[path] = lib
@@ -152,13 +152,19 @@ class Oracle:
             raise OracleError(rc, "greedy_step")
         return tok
 
-    def decode(self, asr, mode, lam, start: int = 0, nthreads: int = 1):
-        """Greedy decode of ``asr`` [B, T, C]: per-frame labels and states after each frame."""
+    def decode(self, asr, mode, lam, starts=None, nthreads: int = 1):
+        """Greedy decode of ``asr`` [B, T, C] from ``starts`` [B] (default: the empty context).
+
+        Returns per-frame labels and the state after each frame, both [B, T]."""
         asr = np.ascontiguousarray(asr, np.float32)
         B, T, C = asr.shape
         labels = np.empty((B, T), np.int32)
         st = np.empty((B, T), np.int32)
-        rc = self._lib.oracle_decode(self._h, _ptr(asr), B, T, C, int(mode), float(lam), int(start),
+        if starts is not None:
+            starts = np.ascontiguousarray(starts, np.int32)
+            assert len(starts) == B
+        rc = self._lib.oracle_decode(self._h, _ptr(asr), B, T, C, int(mode), float(lam),
+                                     _ptr(starts) if starts is not None else None,
                                      _ptr(labels), _ptr(st), int(nthreads))
         if rc != 0:
             raise OracleError(rc, "decode")

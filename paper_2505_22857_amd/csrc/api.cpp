@@ -1,0 +1,230 @@
+// C ABI entry points: argument checks, error reporting, upload and launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "trie.h"
+
+namespace ngpu {
+hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, float *scores, int32_t *next,
+                          hipStream_t stream);
+hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int64_t ld, int mode, float lambda,
+                             int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream);
+}  // namespace ngpu
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int ok() {
+    g_last_error.clear();
+    return NGPU_OK;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(NGPU_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Largest batch whose grid (64 work-items per hypothesis) fits the 32-bit
+// dispatch size.
+constexpr int64_t kMaxBatch = (int64_t(1) << 26) - 256;
+
+ngpu::DevTrie dev_view(const ngpu_lm *lm) {
+    const unsigned char *base = static_cast<const unsigned char *>(lm->dev);
+    ngpu::DevTrie t;
+    t.rec = reinterpret_cast<const ngpu::StateRec *>(base + lm->hdr.off_rec);
+    t.root_w = reinterpret_cast<const float *>(base + lm->hdr.off_root_w);
+    t.root_to = reinterpret_cast<const int32_t *>(base + lm->hdr.off_root_to);
+    t.arc_tok = reinterpret_cast<const int32_t *>(base + lm->hdr.off_arc_tok);
+    t.arc_w = reinterpret_cast<const float *>(base + lm->hdr.off_arc_w);
+    t.arc_to = reinterpret_cast<const int32_t *>(base + lm->hdr.off_arc_to);
+    t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + lm->hdr.off_status);
+    t.num_states = int32_t(lm->S);
+    t.vocab_size = lm->V;
+    t.max_order = lm->N;
+    return t;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ngpu_lm_last_error(void) { return g_last_error.c_str(); }
+
+int ngpu_lm_build(const ngpu_ngram_list *list, int32_t vocab_size, float unk_logprob, uint32_t flags,
+                  ngpu_lm **out) {
+    if (!out) return fail(NGPU_E_INVALID_ARG, "out is null");
+    *out = nullptr;
+    if (!list) return fail(NGPU_E_INVALID_ARG, "list is null");
+    if (flags != 0) return fail(NGPU_E_INVALID_ARG, "flags must be 0");
+    ngpu_lm *lm = new (std::nothrow) ngpu_lm();
+    if (!lm) return fail(NGPU_E_NO_MEMORY, "handle allocation failed");
+    std::string err;
+    int rc;
+    try {
+        rc = ngpu::build_trie(list, vocab_size, unk_logprob, lm, &err);
+    } catch (const std::bad_alloc &) {
+        rc = NGPU_E_NO_MEMORY;
+        err = "host allocation failed while building the trie";
+    }
+    if (rc != NGPU_OK) {
+        delete lm;
+        return fail(rc, "%s", err.c_str());
+    }
+    *out = lm;
+    return ok();
+}
+
+void ngpu_lm_free(ngpu_lm *lm) { delete lm; }
+
+int ngpu_lm_info(const ngpu_lm *lm, ngpu_lm_info_t *out) {
+    if (!lm || !out) return fail(NGPU_E_INVALID_ARG, "null argument");
+    out->num_states = lm->S;
+    out->num_arcs = lm->A;
+    out->max_order = lm->N;
+    out->vocab_size = lm->V;
+    out->device_bytes = int64_t(lm->image.size());
+    return ok();
+}
+
+int ngpu_lm_state_context(const ngpu_lm *lm, int64_t state, int32_t *tokens_out, int32_t *order_out) {
+    if (!lm || !order_out || (!tokens_out && lm->N > 1)) return fail(NGPU_E_INVALID_ARG, "null argument");
+    if (state < 0 || state >= lm->S) return fail(NGPU_E_BAD_STATE, "state %lld outside [0, %lld)",
+                                                 (long long)state, (long long)lm->S);
+    int32_t k = 0;
+    for (int64_t s = state; s != 0; s = lm->state_parent[size_t(s)]) ++k;
+    *order_out = k;
+    int64_t s = state;
+    for (int32_t i = k - 1; i >= 0; --i) {
+        tokens_out[i] = lm->state_tok[size_t(s)];
+        s = lm->state_parent[size_t(s)];
+    }
+    return ok();
+}
+
+size_t ngpu_lm_device_bytes(const ngpu_lm *lm) { return lm ? lm->image.size() : 0; }
+
+int ngpu_lm_upload(ngpu_lm *lm, void *dev_buf, size_t dev_bytes, void *hip_stream) {
+    if (!lm || !dev_buf) return fail(NGPU_E_INVALID_ARG, "null argument");
+    if (reinterpret_cast<uintptr_t>(dev_buf) % ngpu::kAlign != 0)
+        return fail(NGPU_E_INVALID_ARG, "device buffer must be 256-byte aligned");
+    if (dev_bytes < lm->image.size())
+        return fail(NGPU_E_INVALID_ARG, "device buffer has %zu bytes, the image needs %zu", dev_bytes,
+                    lm->image.size());
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, dev_buf);
+    if (e != hipSuccess || attr.type != hipMemoryTypeDevice) {
+        (void)hipGetLastError();
+        return fail(NGPU_E_INVALID_ARG, "dev_buf is not device memory");
+    }
+    e = hipMemcpyAsync(dev_buf, lm->image.data(), lm->image.size(), hipMemcpyHostToDevice,
+                       static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (upload)");
+    lm->dev = dev_buf;
+    lm->device = attr.device;
+    return ok();
+}
+
+int ngpu_lm_advance(const ngpu_lm *lm, const int32_t *d_states, int64_t B, float *d_scores, int32_t *d_next,
+                    void *hip_stream) {
+    if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld outside [0, %lld]", (long long)B,
+                                            (long long)kMaxBatch);
+    if (B == 0) return ok();
+    if (!d_states || !d_scores || !d_next) return fail(NGPU_E_INVALID_ARG, "null device pointer");
+    const ngpu::DevTrie t = dev_view(lm);
+    hipError_t e = ngpu::launch_advance(t, d_states, B, d_scores, d_next, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "advance launch");
+    return ok();
+}
+
+int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t asr_ld, int32_t mode,
+                              float lambda, int32_t *d_states, int32_t *d_prev, int32_t *d_tokens,
+                              void *hip_stream) {
+    if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_TRANSDUCER)
+        return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
+    if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld outside [0, %lld]", (long long)B,
+                                            (long long)kMaxBatch);
+    const int64_t need = mode == NGPU_FUSION_PLAIN ? lm->V : int64_t(lm->V) + 1;
+    if (asr_ld < need) return fail(NGPU_E_INVALID_ARG, "asr_ld %lld < %lld", (long long)asr_ld, (long long)need);
+    if (!std::isfinite(lambda)) return fail(NGPU_E_INVALID_ARG, "lambda must be finite");
+    if (B == 0) return ok();
+    if (!d_asr || !d_states || !d_tokens || (mode == NGPU_FUSION_CTC && !d_prev))
+        return fail(NGPU_E_INVALID_ARG, "null device pointer");
+    const ngpu::DevTrie t = dev_view(lm);
+    hipError_t e = ngpu::launch_fused_step(t, d_asr, B, asr_ld, mode, lambda, d_states, d_prev, d_tokens,
+                                           static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "fused step launch");
+    return ok();
+}
+
+int ngpu_lm_check_states(const ngpu_lm *lm, void *hip_stream, int64_t *bad_count) {
+    if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    int32_t host[4] = {0, 0, 0, 0};
+    void *dstatus = static_cast<unsigned char *>(lm->dev) + lm->hdr.off_status;
+    hipError_t e = hipMemcpyAsync(host, dstatus, sizeof host, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_fail(e, "reading the status word");
+    if (host[0] != 0) {
+        const int32_t zero[4] = {0, 0, 0, 0};
+        e = hipMemcpyAsync(dstatus, zero, sizeof zero, hipMemcpyHostToDevice, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(e, "clearing the status word");
+    }
+    if (bad_count) *bad_count = host[0];
+    if (host[0] != 0) return fail(NGPU_E_BAD_STATE, "%d out-of-range input states", host[0]);
+    return ok();
+}
+
+int ngpu_lm_host_image(const ngpu_lm *lm, const void **data, size_t *bytes) {
+    if (!lm || !data || !bytes) return fail(NGPU_E_INVALID_ARG, "null argument");
+    *data = lm->image.data();
+    *bytes = lm->image.size();
+    return ok();
+}
+
+int ngpu_lm_query_bytes(const ngpu_lm *lm, const int32_t *h_states, int64_t B, int64_t *hbm_bytes,
+                        int64_t *total_bytes) {
+    if (!lm || (B > 0 && !h_states) || !hbm_bytes || !total_bytes) return fail(NGPU_E_INVALID_ARG, "null argument");
+    const ngpu::StateRec *rec = lm->rec();
+    // order-1 states are the ids [state_first[1], state_first[2]) (to S when N = 2)
+    const int64_t order1_end = lm->N == 1 ? 1 : (lm->N == 2 ? lm->S : lm->state_first[2]);
+    int64_t hbm = 0, total = 0;
+    for (int64_t b = 0; b < B; ++b) {
+        int64_t s = h_states[b];
+        if (s < 0 || s >= lm->S) return fail(NGPU_E_BAD_STATE, "state %lld out of range", (long long)s);
+        int64_t h = 8 * int64_t(lm->V), x = 8 * int64_t(lm->V);
+        for (int lvl = 0; lvl < lm->N && s != 0; ++lvl) {
+            const int64_t bytes = 16 + 12 * int64_t(rec[s].end - rec[s].begin);
+            if (s < order1_end) x += bytes;  // order-1 state: shared, cache resident
+            else h += bytes;
+            s = rec[s].bto;
+        }
+        hbm += h;
+        total += h + x;
+    }
+    *hbm_bytes = hbm;
+    *total_bytes = total;
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,279 @@
+// Host construction of the trie image from a closed n-gram list (Section 2.2).
+//
+// Every n-gram is packed into a 128-bit key, ceil(log2 V) bits per token with
+// the first token most significant, so that numeric order of keys of one order
+// is lexicographic order of the tuples.  Per order the keys are sorted; a
+// state's id is then 1 + (number of shorter contexts) + its rank, which equals
+// the canonical numbering (order, tuple).  The prefix of an order-k key is
+// key >> bits and its suffix is the low (k-1)*bits bits, so the closure checks,
+// the backoff state (the suffix) and the arc ranges (children share the prefix)
+// are binary searches and scans over the sorted keys.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+
+#include "trie.h"
+
+namespace ngpu {
+namespace {
+
+typedef unsigned __int128 u128;
+
+struct Entry {
+    u128 key;
+    int64_t row;
+};
+
+struct OrderLevel {
+    std::vector<u128> key;        // sorted
+    std::vector<float> w, b;      // weight / backoff in sorted order
+    std::vector<int32_t> prefix;  // rank of the prefix in order k-1 (k >= 2)
+    std::vector<int32_t> suffix;  // rank of the suffix in order k-1 (k >= 2)
+};
+
+int bits_for(int32_t V) {
+    int b = 1;
+    while ((int64_t(1) << b) < V) ++b;
+    return b;
+}
+
+// rank of key in sorted keys, or -1
+int64_t find_rank(const std::vector<u128> &keys, u128 k) {
+    auto it = std::lower_bound(keys.begin(), keys.end(), k);
+    if (it == keys.end() || *it != k) return -1;
+    return it - keys.begin();
+}
+
+std::string tuple_text(u128 key, int k, int bits) {
+    std::string s = "(";
+    for (int i = 0; i < k; ++i) {
+        uint64_t t = uint64_t(key >> (bits * (k - 1 - i))) & ((uint64_t(1) << bits) - 1);
+        if (i) s += ' ';
+        s += std::to_string(t);
+    }
+    return s + ")";
+}
+
+}  // namespace
+
+int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, std::string *err) {
+    const int N = list->max_order;
+    const int64_t M = list->num_ngrams;
+    if (N < 1 || N > NGPU_LM_MAX_ORDER) {
+        *err = "max_order must be in [1, " + std::to_string(NGPU_LM_MAX_ORDER) + "]";
+        return NGPU_E_ORDER_RANGE;
+    }
+    if (V < 1 || V > NGPU_LM_MAX_VOCAB) {
+        *err = "vocab_size must be in [1, " + std::to_string(NGPU_LM_MAX_VOCAB) + "]";
+        return NGPU_E_TOO_LARGE;
+    }
+    const int bits = bits_for(V);
+    if (bits * N > 128) {
+        *err = "ceil(log2 V) * max_order exceeds 128 bits";
+        return NGPU_E_TOO_LARGE;
+    }
+    if (M < 0 || (M > 0 && (!list->order || !list->tokens || !list->logprob || !list->backoff))) {
+        *err = "null n-gram arrays";
+        return NGPU_E_INVALID_ARG;
+    }
+    if (M > int64_t(INT32_MAX) - 1) {
+        *err = "too many n-grams for int32 state and arc ids";
+        return NGPU_E_TOO_LARGE;
+    }
+    const bool has_unk = !std::isnan(unk);
+    if (has_unk && !std::isfinite(unk)) {
+        *err = "unk_logprob must be finite or NaN";
+        return NGPU_E_NONFINITE;
+    }
+
+    // ---- bucket by order, validate, pack keys
+    std::vector<int64_t> count(N + 1, 0);
+    for (int64_t i = 0; i < M; ++i) {
+        int k = list->order[i];
+        if (k < 1 || k > N) {
+            *err = "row " + std::to_string(i) + ": order " + std::to_string(k) + " outside [1, max_order]";
+            return NGPU_E_ORDER_RANGE;
+        }
+        ++count[k];
+    }
+    std::vector<std::vector<Entry>> ent(N + 1);
+    for (int k = 1; k <= N; ++k) ent[k].reserve(count[k]);
+    for (int64_t i = 0; i < M; ++i) {
+        int k = list->order[i];
+        const int32_t *t = list->tokens + i * N;
+        u128 key = 0;
+        for (int j = 0; j < k; ++j) {
+            if (t[j] < 0 || t[j] >= V) {
+                *err = "row " + std::to_string(i) + ": token " + std::to_string(t[j]) + " outside [0, V)";
+                return NGPU_E_TOKEN_RANGE;
+            }
+            key = (key << bits) | u128(uint32_t(t[j]));
+        }
+        if (!std::isfinite(list->logprob[i]) || (k < N && !std::isfinite(list->backoff[i]))) {
+            *err = "row " + std::to_string(i) + ": non-finite weight";
+            return NGPU_E_NONFINITE;
+        }
+        ent[k].push_back({key, i});
+    }
+
+    std::vector<OrderLevel> lv(N + 1);
+    for (int k = 1; k <= N; ++k) {
+        auto &e = ent[k];
+        std::sort(e.begin(), e.end(), [](const Entry &a, const Entry &b) { return a.key < b.key; });
+        OrderLevel &L = lv[k];
+        L.key.resize(e.size());
+        L.w.resize(e.size());
+        L.b.resize(e.size());
+        for (size_t p = 0; p < e.size(); ++p) {
+            if (p && e[p].key == e[p - 1].key) {
+                *err = "duplicate n-gram " + tuple_text(e[p].key, k, bits);
+                return NGPU_E_DUPLICATE_NGRAM;
+            }
+            L.key[p] = e[p].key;
+            L.w[p] = list->logprob[e[p].row];
+            L.b[p] = k < N ? list->backoff[e[p].row] : 0.0f;
+        }
+        std::vector<Entry>().swap(e);
+    }
+    if (!has_unk && int64_t(lv[1].key.size()) < V) {
+        *err = "a token has no unigram and no <unk> weight was given";
+        return NGPU_E_MISSING_UNIGRAM;
+    }
+
+    // ---- closure: prefix and suffix of every order-k n-gram are listed
+    for (int k = 2; k <= N; ++k) {
+        OrderLevel &L = lv[k];
+        const std::vector<u128> &low = lv[k - 1].key;
+        const u128 smask = (u128(1) << (bits * (k - 1))) - 1;
+        const size_t n = L.key.size();
+        L.prefix.resize(n);
+        L.suffix.resize(n);
+        for (size_t p = 0; p < n; ++p) {
+            int64_t pr = find_rank(low, L.key[p] >> bits);
+            if (pr < 0) {
+                *err = "n-gram " + tuple_text(L.key[p], k, bits) + " has no listed prefix";
+                return NGPU_E_MISSING_PREFIX;
+            }
+            int64_t sr = find_rank(low, L.key[p] & smask);
+            if (sr < 0) {
+                *err = "n-gram " + tuple_text(L.key[p], k, bits) + " has no listed suffix";
+                return NGPU_E_MISSING_SUFFIX;
+            }
+            L.prefix[p] = int32_t(pr);
+            L.suffix[p] = int32_t(sr);
+        }
+    }
+
+    // ---- ids: state (k, rank) -> first[k] + rank for k < N; arcs: order k >= 2 at arc_base[k] + rank
+    std::vector<int64_t> first(N + 1, 0), arc_base(N + 2, 0);
+    int64_t S = 1;
+    for (int k = 1; k < N; ++k) {
+        first[k] = S;
+        S += int64_t(lv[k].key.size());
+    }
+    int64_t A = 0;
+    for (int k = 2; k <= N; ++k) {
+        arc_base[k] = A;
+        A += int64_t(lv[k].key.size());
+    }
+    if (S > INT32_MAX || A > INT32_MAX) {
+        *err = "too many states or arcs for int32 ids";
+        return NGPU_E_TOO_LARGE;
+    }
+
+    // ---- image layout
+    ImageHeader h{};
+    h.magic = kImageMagic;
+    h.vocab_size = V;
+    h.max_order = N;
+    h.num_states = S;
+    h.num_arcs = A;
+    size_t off = align_up(sizeof(ImageHeader));
+    h.off_status = off;
+    off = align_up(off + 4 * sizeof(int32_t));
+    h.off_rec = off;
+    off = align_up(off + size_t(S) * sizeof(StateRec));
+    h.off_root_w = off;
+    off = align_up(off + size_t(V) * 4);
+    h.off_root_to = off;
+    off = align_up(off + size_t(V) * 4);
+    h.off_arc_tok = off;
+    off = align_up(off + size_t(A) * 4);
+    h.off_arc_w = off;
+    off = align_up(off + size_t(A) * 4);
+    h.off_arc_to = off;
+    off = align_up(off + size_t(A) * 4);
+    h.total_bytes = off;
+
+    std::vector<unsigned char> img;
+    try {
+        img.assign(off, 0);
+    } catch (const std::bad_alloc &) {
+        *err = "host allocation of the trie image failed";
+        return NGPU_E_NO_MEMORY;
+    }
+    std::memcpy(img.data(), &h, sizeof h);
+    StateRec *rec = reinterpret_cast<StateRec *>(img.data() + h.off_rec);
+    float *root_w = reinterpret_cast<float *>(img.data() + h.off_root_w);
+    int32_t *root_to = reinterpret_cast<int32_t *>(img.data() + h.off_root_to);
+    int32_t *arc_tok = reinterpret_cast<int32_t *>(img.data() + h.off_arc_tok);
+    float *arc_w = reinterpret_cast<float *>(img.data() + h.off_arc_w);
+    int32_t *arc_to = reinterpret_cast<int32_t *>(img.data() + h.off_arc_to);
+
+    // dense row of the empty context (Section 2.2: every token has an arc; missing ones get <unk>)
+    for (int32_t v = 0; v < V; ++v) {
+        root_w[v] = has_unk ? unk : 0.0f;
+        root_to[v] = 0;
+    }
+    for (size_t p = 0; p < lv[1].key.size(); ++p) {
+        int32_t v = int32_t(uint64_t(lv[1].key[p]));
+        root_w[v] = lv[1].w[p];
+        root_to[v] = N > 1 ? int32_t(first[1] + int64_t(p)) : 0;
+    }
+
+    // state records; state 0 has no sparse arcs (its row is dense)
+    rec[0] = StateRec{0, 0, 0.0f, 0};
+    lm->state_parent.assign(size_t(S), 0);
+    lm->state_tok.assign(size_t(S), -1);
+    const uint64_t tmask = (uint64_t(1) << bits) - 1;
+    for (int k = 1; k < N; ++k) {
+        const OrderLevel &L = lv[k];
+        const size_t n = L.key.size();
+        // children of (k, p) are the order-(k+1) n-grams whose prefix rank is p, contiguous
+        const std::vector<int32_t> &cp = lv[k + 1].prefix;
+        size_t c = 0;
+        for (size_t p = 0; p < n; ++p) {
+            size_t c0 = c;
+            while (c < cp.size() && cp[c] == int32_t(p)) ++c;
+            int64_t id = first[k] + int64_t(p);
+            rec[id].begin = int32_t(arc_base[k + 1] + int64_t(c0));
+            rec[id].end = int32_t(arc_base[k + 1] + int64_t(c));
+            rec[id].bw = L.b[p];
+            rec[id].bto = k == 1 ? 0 : int32_t(first[k - 1] + L.suffix[p]);
+            lm->state_parent[id] = k == 1 ? 0 : int32_t(first[k - 1] + L.prefix[p]);
+            lm->state_tok[id] = int32_t(uint64_t(L.key[p]) & tmask);
+        }
+    }
+    // arcs of orders 2..N: token, weight, next state
+    for (int k = 2; k <= N; ++k) {
+        const OrderLevel &L = lv[k];
+        for (size_t p = 0; p < L.key.size(); ++p) {
+            int64_t a = arc_base[k] + int64_t(p);
+            arc_tok[a] = int32_t(uint64_t(L.key[p]) & tmask);
+            arc_w[a] = L.w[p];
+            arc_to[a] = k < N ? int32_t(first[k] + int64_t(p)) : int32_t(first[N - 1] + L.suffix[p]);
+        }
+    }
+
+    lm->V = V;
+    lm->N = N;
+    lm->S = S;
+    lm->A = A;
+    lm->hdr = h;
+    lm->state_first.assign(first.begin(), first.end());
+    lm->image.swap(img);
+    return NGPU_OK;
+}
+
+}  // namespace ngpu

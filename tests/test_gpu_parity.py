@@ -1,0 +1,287 @@
+"""GPU parity of the HIP kernels with the CPU oracle, through the C ABI.
+
+Next states and labels must match bit for bit; scores within 1e-5 nats (the
+kernels take the same fp32 fold as the oracle's fp32 result, so they are
+expected to be bit-exact and the test reports any difference).  Every case
+prints its name before it touches the GPU.
+"""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+import paper_2505_22857_amd as ng  # noqa: E402
+from oracle import MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle  # noqa: E402
+from synth import (CONFIGS, asr_logprobs, generate_model, make_config_model, phrase_states,  # noqa: E402
+                   seed_for, tiny_model, uniform_states)
+
+TOL = 1e-5
+NTHREADS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def case(msg):
+    print(f"[case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="session")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    return torch.device("cuda:0")
+
+
+_PAIRS = {}
+
+
+def pair(key, make):
+    """(model, uploaded library trie, oracle), built once per session."""
+    if key not in _PAIRS:
+        m = make()
+        lm = ng.NgpuLM.from_model(m, shuffle_seed=17).upload("cuda:0")
+        o = Oracle.from_model(m)
+        _PAIRS[key] = (m, lm, o)
+    return _PAIRS[key]
+
+
+def cfg_pair(i):
+    return pair(f"cfg{i}", lambda: make_config_model(i))
+
+
+def run_advance(lm, states_np, dev):
+    st = torch.from_numpy(np.ascontiguousarray(states_np, np.int32)).to(dev)
+    sc, nx = lm.advance(st)
+    torch.cuda.synchronize()
+    return sc.cpu().numpy(), nx.cpu().numpy()
+
+
+def assert_rows(name, sc, nx, o_s32, o_nx):
+    assert np.array_equal(nx, o_nx), f"{name}: next states differ at {np.argwhere(nx != o_nx)[:5]}"
+    d = np.abs(sc.astype(np.float64) - o_s32)
+    assert np.isfinite(sc).all()
+    assert d.max() <= TOL, f"{name}: max |score diff| {d.max()}"
+    inexact = int((sc != o_s32).sum())
+    print(f"  {name}: {sc.shape[0]} rows, max |diff| {d.max():.3g}, non-bit-exact {inexact}", flush=True)
+
+
+def check_advance(name, m, lm, o, states, dev, rows=None):
+    case(f"advance {name} B={len(states)}")
+    sc, nx = run_advance(lm, states, dev)
+    assert lm.check_states() == 0
+    idx = np.arange(len(states)) if rows is None else rows
+    o_s32, o_nx, _ = o.advance(states[idx], nthreads=NTHREADS)
+    assert_rows(name, sc[idx], nx[idx], o_s32, o_nx)
+    return sc, nx
+
+
+# ------------------------------------------------------------------ advance
+
+def test_advance_cfg1_every_state(dev):
+    m, lm, o = cfg_pair(1)
+    check_advance("cfg1 all states", m, lm, o, np.arange(m.num_states, dtype=np.int32), dev)
+
+
+@pytest.mark.parametrize("B", [1, 33, 32 * 64])
+def test_advance_cfg2(dev, B):
+    m, lm, o = cfg_pair(2)
+    check_advance("cfg2", m, lm, o, uniform_states(m, B, seed=seed_for(2) + B), dev)
+
+
+def test_advance_cfg3_deep_phrase_states(dev):
+    m, lm, o = cfg_pair(3)
+    st = phrase_states(m, CONFIGS[3].batch, seed=seed_for(3))
+    check_advance("cfg3 phrase states", m, lm, o, st, dev)
+    check_advance("cfg3 uniform", m, lm, o, uniform_states(m, 1000, seed=seed_for(3) + 1), dev)
+
+
+def test_advance_cfg4_batches_of_512(dev):
+    m, lm, o = cfg_pair(4)
+    for r in range(8):
+        check_advance(f"cfg4 batch {r}", m, lm, o, uniform_states(m, 512, seed=seed_for(4) + r), dev)
+
+
+def test_advance_cfg4_bench_launch_sampled(dev):
+    """The benchmark's launch (128 batches of 512 in one call): sampled rows vs the
+    oracle, and per-row normalisation (a property of the generated model) on every row."""
+    m, lm, o = cfg_pair(4)
+    B = 128 * 512
+    states = uniform_states(m, B, seed=seed_for(4) + 1000)
+    case(f"advance cfg4 B={B}")
+    st = torch.from_numpy(states).to(dev)
+    sc, nx = lm.advance(st)
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    rows = np.random.default_rng(3).choice(B, 2048, replace=False)
+    rows = np.concatenate([rows, [0, B - 1]])
+    o_s32, o_nx, _ = o.advance(states[rows], nthreads=NTHREADS)
+    rt = torch.from_numpy(rows).to(dev)
+    assert_rows("cfg4 B=65536 sampled", sc[rt].cpu().numpy(), nx[rt].cpu().numpy(), o_s32, o_nx)
+    tot = torch.exp(sc.double()).sum(dim=1)
+    assert float((tot - 1).abs().max()) < 1e-5
+    assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
+
+
+@pytest.mark.parametrize("V,N", [(5, 3), (1000, 3), (1025, 4), (4096, 3), (16, 10)])
+def test_advance_odd_shapes(dev, V, N):
+    if N == 10:
+        counts = [V, 120, 200, 200, 180, 160, 140, 120, 100, 80]
+    else:
+        counts = [V, min(V * V // 2, 6 * V)] + [min(V * V // 2, 6 * V)] * (N - 2)
+    m, lm, o = pair(f"V{V}N{N}", lambda: generate_model(V, counts, 1.0, seed=V + N))
+    st = np.arange(m.num_states, dtype=np.int32)
+    if len(st) > 3000:
+        st = uniform_states(m, 3001, seed=1)
+    check_advance(f"V={V} N={N}", m, lm, o, st, dev)
+
+
+def test_advance_unigram_and_unk_models(dev):
+    m, lm, o = pair("n1", lambda: generate_model(77, [77], 1.0, seed=2))
+    check_advance("N=1", m, lm, o, np.zeros(5, np.int32), dev)
+    m, lm, o = pair("unk", lambda: tiny_model(9, 3, seed=21, n_unigrams=6))
+    check_advance("unk", m, lm, o, np.arange(m.num_states, dtype=np.int32), dev)
+
+
+def test_advance_empty_and_out_of_range(dev):
+    m, lm, o = cfg_pair(1)
+    case("advance B=0")
+    sc, nx = lm.advance(torch.zeros(0, dtype=torch.int32, device=dev))
+    assert sc.shape == (0, m.vocab_size)
+    case("advance with out-of-range states")
+    st = np.array([0, -1, m.num_states, 5], np.int32)
+    sc, nx = run_advance(lm, st, dev)
+    assert lm.check_states() == 2
+    assert lm.check_states() == 0          # the count clears
+    assert np.isnan(sc[1]).all() and (nx[1] == -1).all() and (nx[2] == -1).all()
+    o_s32, o_nx, _ = o.advance(st[[0, 3]])
+    assert_rows("valid rows next to bad ones", sc[[0, 3]], nx[[0, 3]], o_s32, o_nx)
+
+
+# ------------------------------------------------------------------ fused step
+
+def gpu_decode(lm, asr_np, mode, lam, starts, dev):
+    """Frame loop over fused_greedy_step; returns labels and states after each frame."""
+    B, T, C = asr_np.shape
+    asr = torch.from_numpy(asr_np).to(dev)
+    st = torch.from_numpy(np.ascontiguousarray(starts, np.int32)).to(dev)
+    prev = torch.full((B,), lm.vocab_size, dtype=torch.int32, device=dev)
+    labels = torch.empty((B, T), dtype=torch.int32, device=dev)
+    states = torch.empty((B, T), dtype=torch.int32, device=dev)
+    tok = torch.empty(B, dtype=torch.int32, device=dev)
+    for t in range(T):
+        lm.fused_greedy_step(asr[:, t, :], lam, st, prev if mode == MODE_CTC else None, mode=mode, tokens=tok)
+        labels[:, t] = tok
+        states[:, t] = st
+    torch.cuda.synchronize()
+    return labels.cpu().numpy(), states.cpu().numpy()
+
+
+def check_decode(name, lm, o, asr, mode, lam, starts, dev):
+    case(f"fused {name} B={asr.shape[0]} T={asr.shape[1]}")
+    gl, gs = gpu_decode(lm, asr, mode, lam, starts, dev)
+    assert lm.check_states() == 0
+    ol, os_ = o.decode(asr, mode, lam, starts, nthreads=NTHREADS)
+    bad = np.argwhere(gl != ol)
+    assert len(bad) == 0, f"{name}: labels differ first at (b, t) = {bad[0]}"
+    assert np.array_equal(gs, os_), f"{name}: states differ"
+    print(f"  {name}: {gl.size} decisions identical", flush=True)
+    return gl, gs
+
+
+def test_fused_plain_cfg1(dev):
+    m, lm, o = cfg_pair(1)
+    spec = CONFIGS[1]
+    asr = asr_logprobs((spec.batch, spec.steps, m.vocab_size), seed=seed_for(1) + 50)
+    check_decode("plain cfg1", lm, o, asr, MODE_PLAIN, spec.lam, np.zeros(spec.batch, np.int32), dev)
+
+
+def test_fused_plain_cfg2_with_advance_every_step(dev):
+    m, lm, o = cfg_pair(2)
+    spec = CONFIGS[2]
+    starts = uniform_states(m, spec.batch, seed=seed_for(2) + 77)
+    asr = asr_logprobs((spec.batch, spec.steps, m.vocab_size), seed=seed_for(2) + 50)
+    gl, gs = check_decode("plain cfg2", lm, o, asr, MODE_PLAIN, spec.lam, starts, dev)
+    # the advance query at every step's states
+    visited = np.concatenate([starts, gs[:, :-1].reshape(-1)]).astype(np.int32)
+    check_advance("cfg2 states along the decode", m, lm, o, visited, dev)
+
+
+def test_fused_ctc_cfg5(dev):
+    m, lm, o = cfg_pair(4)
+    spec = CONFIGS[5]
+    V = m.vocab_size
+    asr = asr_logprobs((spec.batch, spec.steps, V + 1), seed=seed_for(5), blank_boost=spec.blank_boost)
+    gl, _ = check_decode("ctc cfg5", lm, o, asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), dev)
+    blank = (gl == V).mean()
+    print(f"  cfg5: blank labels {blank:.3f}", flush=True)
+
+
+def test_fused_transducer_and_ctc_small(dev):
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    starts = uniform_states(m, 64, seed=5)
+    asr = asr_logprobs((64, 40, V + 1), seed=6, blank_boost=3.0)
+    check_decode("transducer cfg2", lm, o, asr, MODE_TRANSDUCER, 0.7, starts, dev)
+    check_decode("ctc cfg2", lm, o, asr, MODE_CTC, 0.7, starts, dev)
+
+
+def test_fused_ties_lambda_zero_and_all_blank(dev):
+    m, lm, o = cfg_pair(1)
+    V = m.vocab_size
+    B = 65
+    starts = uniform_states(m, B, seed=8)
+    asr = asr_logprobs((B, 6, V + 1), seed=9)
+    asr[:, 0, :] = -3.0                       # full ties in frame 0
+    asr[:5, 1, :] = -5.0
+    asr[:5, 1, V] = -0.01                     # blank wins frame 1 for five rows
+    asr[:, 2, 7] = asr[:, 2, 100] = 2.0       # two-way ties
+    for mode in (MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER):
+        a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+        for lam in (0.0, 0.5, -1.0, 4.0):
+            check_decode(f"ties mode={mode} lambda={lam}", lm, o, a, mode, lam, starts, dev)
+    # an all-blank utterance never moves its state
+    allb = np.full((3, 10, V + 1), -9.0, np.float32)
+    allb[:, :, V] = -0.001
+    gl, gs = check_decode("all blank", lm, o, allb, MODE_CTC, 0.5, starts[:3], dev)
+    assert (gl == V).all() and (gs == starts[:3, None]).all()
+
+
+def test_fused_strided_asr_rows(dev):
+    """asr rows with a leading dimension larger than V + 1."""
+    m, lm, o = cfg_pair(1)
+    V = m.vocab_size
+    base = asr_logprobs((16, V + 1), seed=10, blank_boost=1.0)
+    padded = np.full((16, V + 40), 7.0, np.float32)   # padding must never be read
+    padded[:, :V + 1] = base
+    case("fused with asr_ld = V + 40")
+    st = torch.from_numpy(uniform_states(m, 16, seed=11)).to(dev)
+    st0 = st.cpu().numpy().copy()
+    prev = torch.full((16,), V, dtype=torch.int32, device=dev)
+    tok = lm.fused_greedy_step(torch.from_numpy(padded).to(dev), 0.5, st, prev, mode=ng.NGPU_FUSION_CTC)
+    torch.cuda.synchronize()
+    o_st = st0.copy()
+    o_prev = np.full(16, V, np.int32)
+    o_tok = o.greedy_step(base, MODE_CTC, 0.5, o_st, o_prev)
+    assert np.array_equal(tok.cpu().numpy(), o_tok)
+    assert np.array_equal(st.cpu().numpy(), o_st)
+    assert np.array_equal(prev.cpu().numpy(), o_prev)
+
+
+def test_fused_out_of_range_state(dev):
+    m, lm, o = cfg_pair(1)
+    V = m.vocab_size
+    case("fused with an out-of-range state")
+    st = torch.tensor([3, m.num_states + 5, 0], dtype=torch.int32, device=dev)
+    asr = torch.from_numpy(asr_logprobs((3, V), seed=12)).to(dev)
+    tok = lm.fused_greedy_step(asr, 0.5, st)
+    torch.cuda.synchronize()
+    assert lm.check_states() == 1
+    t = tok.cpu().numpy()
+    assert t[1] == -1 and int(st[1]) == m.num_states + 5
+    o_st = np.array([3, 0], np.int32)
+    o_tok = o.greedy_step(asr.cpu().numpy()[[0, 2]], MODE_PLAIN, 0.5, o_st)
+    assert t[[0, 2]].tolist() == o_tok.tolist()

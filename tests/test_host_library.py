@@ -1,0 +1,205 @@
+"""Host side of the C-ABI library: exports, trie construction, numbering, errors.
+
+None of these tests launches a kernel.  ``test_image_walk_matches_oracle``
+walks the host copy of the trie image on the CPU, as Algorithm 1 states it, to
+check the builder's arrays against the oracle before any GPU is involved.
+"""
+
+import ctypes
+import os
+import re
+import struct
+
+import numpy as np
+import pytest
+
+import paper_2505_22857_amd as ng
+from oracle import Oracle
+from synth import generate_model, make_config_model, tiny_model, uniform_states
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ngpu_lm.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return ng.load_library()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ngpu_lm_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol(lib):
+    decl = declared_functions()
+    assert len(decl) >= 10
+    for name in decl:
+        assert hasattr(lib, name), name
+    assert sorted(ng.EXPORTED) == decl
+
+
+def parse_image(img):
+    hdr = struct.unpack_from("<IiiiqqQQQQQQQQ", img.tobytes()[:128])
+    magic, V, N, _, S, A, o_rec, o_rw, o_rt, o_tok, o_w, o_to, o_st, total = hdr
+    assert magic == 0x4D4C504E and total == len(img)
+    rec = np.frombuffer(img, np.int32, 4 * S, o_rec).reshape(S, 4)
+    return dict(V=V, N=N, S=S, A=A,
+                begin=rec[:, 0], end=rec[:, 1], bw=rec[:, 2].view(np.float32), bto=rec[:, 3],
+                root_w=np.frombuffer(img, np.float32, V, o_rw), root_to=np.frombuffer(img, np.int32, V, o_rt),
+                tok=np.frombuffer(img, np.int32, A, o_tok), w=np.frombuffer(img, np.float32, A, o_w),
+                to=np.frombuffer(img, np.int32, A, o_to))
+
+
+def walk_image(im, s):
+    """Algorithm 1 over the image arrays, in fp32."""
+    V = im["V"]
+    nxt = np.full(V, -1, np.int32)
+    sc = np.zeros(V, np.float32)
+    acc = np.float32(0.0)
+    while s != 0:
+        b, e = im["begin"][s], im["end"][s]
+        toks = im["tok"][b:e]
+        unset = nxt[toks] == -1
+        sc[toks[unset]] = acc + im["w"][b:e][unset]
+        nxt[toks[unset]] = im["to"][b:e][unset]
+        acc = np.float32(acc + im["bw"][s])
+        s = im["bto"][s]
+    unset = nxt == -1
+    sc[unset] = acc + im["root_w"][unset]
+    nxt[unset] = im["root_to"][unset]
+    return sc, nxt
+
+
+@pytest.mark.parametrize("which", ["cfg1", "cfg2", "tiny-unk", "n1", "n2", "n10"])
+def test_image_walk_matches_oracle(which):
+    if which == "cfg1":
+        m, states = make_config_model(1), None
+    elif which == "cfg2":
+        m = make_config_model(2)
+        states = uniform_states(m, 300, seed=2)
+    elif which == "tiny-unk":
+        m, states = tiny_model(9, 3, seed=21, n_unigrams=6), None
+    elif which == "n1":
+        m, states = generate_model(40, [40], 1.0, seed=1), None
+    elif which == "n2":
+        m, states = generate_model(40, [40, 400], 1.0, seed=1), None
+    else:
+        m = generate_model(16, [16, 120, 200, 200, 180, 160, 140, 120, 100, 80], 1.0, seed=3)
+        states = None
+    lm = ng.NgpuLM.from_model(m, shuffle_seed=7)
+    o = Oracle.from_model(m)
+    assert lm.num_states == o.num_states == m.num_states
+    if states is None:
+        states = np.arange(m.num_states, dtype=np.int32)
+    im = parse_image(lm.host_image())
+    s32, nx, _ = o.advance(states, nthreads=4)
+    for i, s in enumerate(states):
+        sc, n = walk_image(im, int(s))
+        assert np.array_equal(n, nx[i]), (which, s)
+        assert np.array_equal(sc, s32[i]), (which, s)   # same fp32 fold: bit-exact
+
+
+def test_numbering_matches_oracle_on_shuffled_lists():
+    for idx in (1, 2):
+        m = make_config_model(idx)
+        lm = ng.NgpuLM.from_model(m, shuffle_seed=idx)
+        o = Oracle.from_model(m, shuffle_seed=idx + 10)
+        S = lm.num_states
+        ids = range(S) if S < 5000 else np.random.default_rng(0).integers(0, S, 3000)
+        for s in ids:
+            assert lm.state_context(int(s)) == o.state_context(int(s))
+
+
+def test_csr_rows_sorted_and_consistent():
+    m = make_config_model(2)
+    lm = ng.NgpuLM.from_model(m)
+    im = parse_image(lm.host_image())
+    b, e = im["begin"], im["end"]
+    assert b[0] == e[0] == 0
+    assert (e >= b).all() and (b[1:] >= 0).all() and (e <= im["A"]).all()
+    # one contiguous range per state, in state order, covering every arc
+    assert b[1] == 0 and (b[2:] == e[1:-1]).all() and e[-1] == im["A"]
+    for s in np.random.default_rng(1).integers(1, im["S"], 500):
+        t = im["tok"][b[s]:e[s]]
+        assert (np.diff(t) > 0).all()
+    # arcs of orders below N lead to the arc's own state, i.e. id = arc index + a constant
+    n_low = sum(m.counts[1:-1])
+    to = im["to"][:n_low]
+    assert (np.diff(to) == 1).all()
+
+
+def _raw_build(V, N, order, tokens, W, B, unk=float("nan"), flags=0):
+    lib = ng.load_library()
+    order = np.ascontiguousarray(order, np.int32)
+    tokens = np.ascontiguousarray(tokens, np.int32)
+    W = np.ascontiguousarray(W, np.float32)
+    B = np.ascontiguousarray(B, np.float32)
+    lst = ng._NgramList(len(order), N, order.ctypes.data, tokens.ctypes.data, W.ctypes.data, B.ctypes.data)
+    h = ctypes.c_void_p()
+    rc = lib.ngpu_lm_build(ctypes.byref(lst), V, unk, flags, ctypes.byref(h))
+    if rc == 0:
+        lib.ngpu_lm_free(h)
+    return rc, lib.ngpu_lm_last_error().decode()
+
+
+def _fig1():
+    order = np.array([1, 1, 1, 2, 2, 3], np.int32)
+    tokens = np.array([[0, -1, -1], [1, -1, -1], [2, -1, -1], [0, 1, -1], [1, 2, -1], [0, 1, 2]], np.int32)
+    W = np.array([-1, -1, -1, -0.5, -0.5, -0.1], np.float32)
+    B = np.array([-0.3, -0.3, -0.3, -0.2, -0.2, 0], np.float32)
+    return order, tokens, W, B
+
+
+def test_build_error_codes():
+    o, t, W, B = _fig1()
+    assert _raw_build(3, 3, o, t, W, B)[0] == 0
+    assert _raw_build(3, 3, np.append(o, 2), np.vstack([t, t[3]]), np.append(W, 0), np.append(B, 0))[0] == -4
+    bad = t.copy(); bad[1, 0] = 3
+    assert _raw_build(3, 3, o, bad, W, B)[0] == -2
+    bad = o.copy(); bad[0] = 4
+    assert _raw_build(3, 3, bad, t, W, B)[0] == -3
+    assert _raw_build(3, 11, o, np.pad(t, ((0, 0), (0, 8)), constant_values=-1), W, B)[0] == -3
+    # trigram (0 1 2) without its prefix (0 1)
+    keep = np.array([1, 1, 1, 0, 1, 1], bool)
+    assert _raw_build(3, 3, o[keep], t[keep], W[keep], B[keep])[0] == -5
+    # trigram (0 1 2) without its suffix (1 2)
+    keep = np.array([1, 1, 1, 1, 0, 1], bool)
+    assert _raw_build(3, 3, o[keep], t[keep], W[keep], B[keep])[0] == -6
+    # a token with no unigram: error without <unk>, fine with it
+    assert _raw_build(4, 3, o, t, W, B)[0] == -7
+    assert _raw_build(4, 3, o, t, W, B, unk=-5.0)[0] == 0
+    Wn = W.copy(); Wn[2] = np.nan
+    assert _raw_build(3, 3, o, t, Wn, B)[0] == -10
+    assert _raw_build(ng.MAX_VOCAB + 1, 3, o, t, W, B)[0] == -11
+    assert _raw_build(3, 3, o, t, W, B, flags=1)[0] == -1
+
+
+def test_queries_before_upload_fail_cleanly():
+    m = make_config_model(1)
+    lm = ng.NgpuLM.from_model(m)
+    lib = ng.load_library()
+    assert lib.ngpu_lm_advance(lm._h, None, 4, None, None, None) == -8
+    assert lib.ngpu_lm_fused_greedy_step(lm._h, None, 4, 129, 0, 0.5, None, None, None, None) == -8
+    n = ctypes.c_int64()
+    assert lib.ngpu_lm_check_states(lm._h, None, ctypes.byref(n)) == -8
+    assert "not uploaded" in lib.ngpu_lm_last_error().decode()
+
+
+def test_query_bytes():
+    m = make_config_model(1)
+    lm = ng.NgpuLM.from_model(m)
+    V = m.vocab_size
+    hbm, tot = lm.query_bytes(np.zeros(3, np.int32))
+    assert hbm == 3 * 8 * V and tot == 3 * 16 * V
+    im = parse_image(lm.host_image())
+    s = m.state_offset(2) + 5                      # an order-2 state: its record and arcs are HBM traffic
+    deg2 = im["end"][s] - im["begin"][s]
+    s1 = im["bto"][s]
+    deg1 = im["end"][s1] - im["begin"][s1]
+    hbm, tot = lm.query_bytes(np.array([s], np.int32))
+    assert hbm == 8 * V + 16 + 12 * deg2
+    assert tot == hbm + 8 * V + 16 + 12 * deg1
+    with pytest.raises(ng.NgpuError):
+        lm.query_bytes(np.array([m.num_states], np.int32))

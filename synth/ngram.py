@@ -19,10 +19,14 @@ Model recipe (all randomness from one ``numpy.random.Generator``):
   mass ``m_c ~ U(0.5, 0.95)`` (``1`` when ``E(c)`` covers the vocabulary) is
   split over ``E(c)`` in proportion to ``P(v | c[1:]) * exp(N(0, 1))``.  With
   ``l_c = sum_{v in E(c)} P(v | c[1:])`` (every term explicit by suffix
-  closure) the backoff weight ``B(c) = ln(1 - m_c) - ln(1 - l_c)`` makes
+  closure) and ``Z(c[1:])`` the total mass of the shorter context as stored,
+  the backoff weight ``B(c) = ln(1 - m_c) - ln(Z(c[1:]) - l_c)`` makes
   ``sum_v P(v | c) = 1`` under the backoff rule W(t|c) = B(c) + W(t|c[1:])
   (Section 2.1).  Weights are rounded to fp32 first and the backoff is computed
-  from the rounded values, so the stored model is normalised to ~1e-7.
+  from the rounded values and the stored mass Z of the shorter context (not
+  from an assumed 1: when ``1 - l_c`` is small, the rounding residue of the
+  shorter context would otherwise be amplified by ``1 / (1 - l_c)``), so the
+  stored model is normalised to ~1e-7 at every depth.
 
 All weights are natural logarithms.  The model is kept per order as a trie
 level: ``pid`` (row of the prefix in the order below), ``tok`` (last token),
@@ -244,8 +248,13 @@ def _select_candidates(prev: Level, grand_n: int, need: int, forced: np.ndarray,
 
 
 def _assign_probabilities(prev: Level, pid: np.ndarray, sid: np.ndarray, V: int,
-                          rng: np.random.Generator):
-    """Weights of the new level and backoff weights of its contexts (the previous level)."""
+                          z_low: np.ndarray, rng: np.random.Generator):
+    """Weights of the new level; backoff weights and stored mass Z of its contexts.
+
+    ``z_low[c]`` is the stored mass of context c's suffix c[1:].  Sets
+    ``prev.B`` and returns ``(W, Z)`` with Z the stored mass of each context of
+    the previous level under the backoff rule.
+    """
     n_prev = len(prev.tok)
     p_low = np.exp(prev.W[sid].astype(np.float64))        # explicit by suffix closure
     raw = p_low * np.exp(rng.standard_normal(len(pid)))
@@ -260,10 +269,13 @@ def _assign_probabilities(prev: Level, pid: np.ndarray, sid: np.ndarray, V: int,
     m32 = np.bincount(pid, weights=np.exp(W.astype(np.float64)), minlength=n_prev)
     B = np.zeros(n_prev)
     has = (cnt > 0) & ~full
-    compl = np.maximum(1.0 - l[has], 1e-12)
+    compl = np.maximum(z_low[has] - l[has], 1e-12)        # mass left to the backoff
     B[has] = np.log1p(-np.minimum(m32[has], 1.0 - 1e-12)) - np.log(compl)
     prev.B = B.astype(np.float32)
-    return W
+    Z = z_low.copy()                                       # no continuations: all mass backs off
+    Z[full] = m32[full]
+    Z[has] = m32[has] + np.exp(prev.B[has].astype(np.float64)) * compl
+    return W, Z
 
 
 def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
@@ -281,6 +293,10 @@ def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
                 W=W1, B=np.zeros(len(toks), np.float32), cum=W1.astype(np.float64))
     model = NgramModel(vocab_size=V, max_order=N, levels=[root, lv1], unk_logprob=unk,
                        phrases=[np.asarray(p, np.int64) for p in phrases] if phrases is not None else None)
+    z_root = float(np.exp(W1.astype(np.float64)).sum())
+    if not np.isnan(unk):
+        z_root += (V - len(toks)) * float(np.exp(np.float64(np.float32(unk))))
+    z_levels = [np.array([z_root])]                        # Z per context, level by level
     for k in range(2, N + 1):
         prev = model.levels[k - 1]
         grand_n = len(model.levels[k - 2].tok)
@@ -301,7 +317,10 @@ def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
         tok = prev.tok[sid]
         order = np.lexsort((tok, pid))
         pid, sid, tok = pid[order], sid[order], tok[order]
-        W = _assign_probabilities(prev, pid, sid, V, rng)
+        # stored mass of each context's suffix: Z of the level below (the root for unigrams)
+        z_low = z_levels[k - 2][prev.sid]
+        W, z_prev = _assign_probabilities(prev, pid, sid, V, z_low, rng)
+        z_levels.append(z_prev)
         cum = prev.cum[pid] + W.astype(np.float64)
         model.levels.append(Level(pid=pid, tok=tok.astype(np.int32), sid=sid, W=W,
                                   B=np.zeros(len(tok), np.float32), cum=cum))

@@ -17,22 +17,24 @@ def _closure_ok(model):
         assert (np.diff(model.levels[k].pid * model.vocab_size + model.levels[k].tok) > 0).all()
 
 
-def _construction_identity(model, tol=2e-6):
-    """sum_E P(v|c) + exp(B(c)) * (1 - sum_E P(v|c[1:])) = 1 for every context."""
+def _construction_identity(model, tol=1e-6):
+    """Stored mass Z(c) = sum_E P(v|c) + exp(B(c)) * (Z(c[1:]) - sum_E P(v|c[1:])) is 1 for every context."""
     V = model.vocab_size
+    z1 = np.exp(model.levels[1].W.astype(np.float64)).sum()
+    if not np.isnan(model.unk_logprob):
+        z1 += (V - len(model.levels[1].tok)) * np.exp(np.float64(model.unk_logprob))
+    assert abs(z1 - 1.0) < 1e-6
+    z = [np.array([z1])]
     for k in range(2, model.max_order + 1):
         lv, prev = model.levels[k], model.levels[k - 1]
         n = len(prev.tok)
         m = np.bincount(lv.pid, weights=np.exp(lv.W.astype(np.float64)), minlength=n)
         l = np.bincount(lv.pid, weights=np.exp(prev.W[lv.sid].astype(np.float64)), minlength=n)
-        cnt = np.bincount(lv.pid, minlength=n)
-        tot = m + np.exp(prev.B.astype(np.float64)) * (1.0 - l)
-        sel = cnt < V
-        assert np.abs(tot[sel] - 1.0).max() < tol
-    p1 = np.exp(model.levels[1].W.astype(np.float64)).sum()
-    if not np.isnan(model.unk_logprob):
-        p1 += (V - len(model.levels[1].tok)) * np.exp(np.float64(model.unk_logprob))
-    assert abs(p1 - 1.0) < 1e-6
+        zlow = z[-1][prev.sid]
+        tot = m + np.exp(prev.B.astype(np.float64)) * (zlow - l)
+        tot[np.bincount(lv.pid, minlength=n) == V] = m[np.bincount(lv.pid, minlength=n) == V]
+        assert np.abs(tot - 1.0).max() < tol, (k, np.abs(tot - 1.0).max())
+        z.append(tot)
 
 
 def test_config_counts_and_closure():

@@ -195,17 +195,18 @@ def main():
         from oracle import Oracle
         cores = len(os.sched_getaffinity(0))
         o = Oracle.from_model(model)
-        probe = states_np[:256]
+        probe = states_np[:4096]
         t0 = time.perf_counter()
         o.advance(probe, nthreads=cores)
         dt = time.perf_counter() - t0
-        n = int(min(B, max(256, args.cpu_seconds / max(dt, 1e-6) * 256)))
-        sample = states_np[:n]
+        n = int(min(1 << 22, max(4096, args.cpu_seconds / max(dt, 1e-6) * len(probe))))
+        sample = uniform_states(model, n, seed=seed_for(4) + 1000)   # starts with the benchmark states
         t0 = time.perf_counter()
         o.advance(sample, nthreads=cores)
         dt = time.perf_counter() - t0
         cpu = {"value": n * V / dt, "unit": "scores/s", "cores": cores, "kind": "oracle",
-               "sample": f"first {n} of the {B} benchmark states, full {V}-token rows, {dt:.1f}s"}
+               "sample": f"{n} uniform states of the same model (the benchmark draw extended), "
+                         f"full {V}-token rows, {dt:.1f}s"}
         log(f"oracle: {cpu['value']:.3g} scores/s on {cores} cores")
         del o
 

@@ -159,12 +159,13 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
 int ngpu_lm_check_states(const ngpu_lm *lm, void *hip_stream, int64_t *bad_count);
 
 /* Algorithmic memory traffic of ngpu_lm_advance on host-side states h_states[B]:
- *   *hbm_bytes   = 8V (output row) + sum over the chain states of order >= 2
- *                  of (16-byte record + 12 bytes per arc),
- *   *total_bytes = *hbm_bytes + 8V (dense empty-context row) + the order-1
- *                  state's record and arcs,
- * summed over the batch.  The order-1 rows and the dense row are shared by all
- * hypotheses and stay in the caches, hence the two figures.  Host-only. */
+ *   *hbm_bytes   = 8V (output row) + the state's chain record (16 bytes per
+ *                  order, 16 for state 0) + 12 bytes per arc of each state of
+ *                  order >= 2 on its backoff chain,
+ *   *total_bytes = *hbm_bytes + 8V (the dense row of the order-1 ancestor, or
+ *                  of the empty context),
+ * summed over the batch.  The dense rows are shared by all hypotheses and
+ * mostly served from the caches, hence the two figures.  Host-only. */
 int ngpu_lm_query_bytes(const ngpu_lm *lm, const int32_t *h_states, int64_t B,
                         int64_t *hbm_bytes, int64_t *total_bytes);
 

@@ -1,13 +1,12 @@
 // Batched full-vocabulary backoff query (Algorithm 1, batched over hypotheses).
 //
 // Grid: one wavefront per hypothesis, HPB wavefronts per workgroup, each with
-// its own V-wide score/state row in LDS (8 bytes per token).  After the walk,
-// the row is written to HBM with 16-byte stores (when V is a multiple of 4):
-// lane l covers tokens 4l..4l+3 of each 256-token stripe, so one store
-// instruction of the wavefront writes 1 KiB contiguously.  Unset slots take
-// the dense empty-context row plus the accumulated backoff (the last level of
-// Algorithm 1).  No MFMA: the work is gathers, scatters and one fp32 add per
-// token.
+// its own V-wide score/state row in LDS (8 bytes per token).  After the
+// sparse levels are scattered, the row is merged with the order-1 ancestor's
+// dense row and written to HBM with 16-byte stores (when V is a multiple of
+// 4): lane l covers tokens 4l..4l+3 of each 256-token stripe, so one store
+// instruction of the wavefront writes 1 KiB contiguously.  No MFMA: the work
+// is gathers, scatters and one fp32 add per token.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -21,7 +20,7 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
                                                                int64_t B, float *__restrict__ scores,
                                                                int32_t *__restrict__ next) {
     extern __shared__ float lds[];
-    const int wave = threadIdx.x / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
     const int64_t b = int64_t(blockIdx.x) * HPB + wave;
     if (b >= B) return;  // whole wavefronts leave; no workgroup barrier is used
@@ -40,29 +39,30 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
         }
         return;
     }
-    const float acc = walk_into_lds(t, s, ls, ln, lane);
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
+    const float *dw = t.dense_w + size_t(h.dense_row) * V;
+    const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
 
     if (VEC) {
         for (int v = lane * 4; v < V; v += 4 * kWave) {
-            int4 n = *reinterpret_cast<const int4 *>(ln + v);
-            float4 x = *reinterpret_cast<const float4 *>(ls + v);
-            const float4 rw = *reinterpret_cast<const float4 *>(t.root_w + v);
-            const int4 rt = *reinterpret_cast<const int4 *>(t.root_to + v);
-            if (n.x < 0) { x.x = acc + rw.x; n.x = rt.x; }
-            if (n.y < 0) { x.y = acc + rw.y; n.y = rt.y; }
-            if (n.z < 0) { x.z = acc + rw.z; n.z = rt.z; }
-            if (n.w < 0) { x.w = acc + rw.w; n.w = rt.w; }
-            *reinterpret_cast<float4 *>(orow + v) = x;
-            *reinterpret_cast<int4 *>(nrow + v) = n;
+            const int4 n4 = *reinterpret_cast<const int4 *>(ln + v);
+            const float4 x4 = *reinterpret_cast<const float4 *>(ls + v);
+            const float4 w4 = *reinterpret_cast<const float4 *>(dw + v);
+            const int4 t4 = *reinterpret_cast<const int4 *>(dt + v);
+            float4 xo;
+            int4 no;
+            merge_slot(h, x4.x, n4.x, w4.x, t4.x, xo.x, no.x);
+            merge_slot(h, x4.y, n4.y, w4.y, t4.y, xo.y, no.y);
+            merge_slot(h, x4.z, n4.z, w4.z, t4.z, xo.z, no.z);
+            merge_slot(h, x4.w, n4.w, w4.w, t4.w, xo.w, no.w);
+            *reinterpret_cast<float4 *>(orow + v) = xo;
+            *reinterpret_cast<int4 *>(nrow + v) = no;
         }
     } else {
         for (int v = lane; v < V; v += kWave) {
-            int n = ln[v];
-            float x = ls[v];
-            if (n < 0) {
-                x = acc + t.root_w[v];
-                n = t.root_to[v];
-            }
+            float x;
+            int n;
+            merge_slot(h, ls[v], ln[v], dw[v], dt[v], x, n);
             orow[v] = x;
             nrow[v] = n;
         }

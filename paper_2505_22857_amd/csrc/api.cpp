@@ -45,17 +45,21 @@ constexpr int64_t kMaxBatch = (int64_t(1) << 26) - 256;
 
 ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     const unsigned char *base = static_cast<const unsigned char *>(lm->dev);
+    const ngpu::ImageHeader &h = lm->hdr;
     ngpu::DevTrie t;
-    t.rec = reinterpret_cast<const ngpu::StateRec *>(base + lm->hdr.off_rec);
-    t.root_w = reinterpret_cast<const float *>(base + lm->hdr.off_root_w);
-    t.root_to = reinterpret_cast<const int32_t *>(base + lm->hdr.off_root_to);
-    t.arc_tok = reinterpret_cast<const int32_t *>(base + lm->hdr.off_arc_tok);
-    t.arc_w = reinterpret_cast<const float *>(base + lm->hdr.off_arc_w);
-    t.arc_to = reinterpret_cast<const int32_t *>(base + lm->hdr.off_arc_to);
-    t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + lm->hdr.off_status);
+    t.chain = base + h.off_chain;
+    t.dense_w = reinterpret_cast<const float *>(base + h.off_dense_w);
+    t.dense_to = reinterpret_cast<const int32_t *>(base + h.off_dense_to);
+    t.arc_tok = reinterpret_cast<const int32_t *>(base + h.off_arc_tok);
+    t.arc_w = reinterpret_cast<const float *>(base + h.off_arc_w);
+    t.arc_to = reinterpret_cast<const int32_t *>(base + h.off_arc_to);
+    t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + h.off_status);
     t.num_states = int32_t(lm->S);
     t.vocab_size = lm->V;
     t.max_order = lm->N;
+    t.pad = 0;
+    for (int k = 0; k <= NGPU_LM_MAX_ORDER; ++k) t.first[k] = h.first[k];
+    for (int k = 0; k < NGPU_LM_MAX_ORDER; ++k) t.off_order[k] = h.off_order[k];
     return t;
 }
 
@@ -205,22 +209,21 @@ int ngpu_lm_host_image(const ngpu_lm *lm, const void **data, size_t *bytes) {
 int ngpu_lm_query_bytes(const ngpu_lm *lm, const int32_t *h_states, int64_t B, int64_t *hbm_bytes,
                         int64_t *total_bytes) {
     if (!lm || (B > 0 && !h_states) || !hbm_bytes || !total_bytes) return fail(NGPU_E_INVALID_ARG, "null argument");
-    const ngpu::StateRec *rec = lm->rec();
-    // order-1 states are the ids [state_first[1], state_first[2]) (to S when N = 2)
-    const int64_t order1_end = lm->N == 1 ? 1 : (lm->N == 2 ? lm->S : lm->state_first[2]);
+    const int64_t V = lm->V;
     int64_t hbm = 0, total = 0;
     for (int64_t b = 0; b < B; ++b) {
         int64_t s = h_states[b];
         if (s < 0 || s >= lm->S) return fail(NGPU_E_BAD_STATE, "state %lld out of range", (long long)s);
-        int64_t h = 8 * int64_t(lm->V), x = 8 * int64_t(lm->V);
-        for (int lvl = 0; lvl < lm->N && s != 0; ++lvl) {
-            const int64_t bytes = 16 + 12 * int64_t(rec[s].end - rec[s].begin);
-            if (s < order1_end) x += bytes;  // order-1 state: shared, cache resident
-            else h += bytes;
-            s = rec[s].bto;
+        int k = 0;   // order of s
+        for (int j = 1; j < lm->N; ++j)
+            if (s >= lm->hdr.first[j]) k = j;
+        int64_t bytes = 8 * V + 16 * (k > 0 ? k : 1);   // output row + chain record
+        for (int j = 0; j < k - 1; ++j) {                // sparse levels: orders k..2
+            bytes += 12 * int64_t(lm->rec[size_t(s)].end - lm->rec[size_t(s)].begin);
+            s = lm->rec[size_t(s)].bto;
         }
-        hbm += h;
-        total += h + x;
+        hbm += bytes;
+        total += bytes + 8 * V;                          // + the shared dense row
     }
     *hbm_bytes = hbm;
     *total_bytes = total;

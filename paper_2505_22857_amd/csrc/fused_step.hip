@@ -4,11 +4,11 @@
 // ASR argmax over the V + 1 classes; when that keeps blank (or, for CTC, the
 // previous label) the LM is not consulted at all and the state stays.
 // Otherwise the wavefront walks its state's backoff chain into an LDS row (the
-// same walk as the advance kernel, with no HBM write of the row), forms
-// fmaf(lambda, lm[v], asr[v]) per token and reduces to the argmax with
-// lowest-index ties through 64-bit keys (value, ~index) and cross-lane
-// shuffles.  The winner's next state comes from the LDS row or the dense
-// empty-context row.  No MFMA: one fma and one compare per token.
+// same walk as the advance kernel, with no HBM write of the row), merges the
+// dense row of the order-1 ancestor, forms fmaf(lambda, lm[v], asr[v]) per
+// token and reduces to the argmax with lowest-index ties through 64-bit keys
+// (value, ~index) and cross-lane shuffles.  The winner's next state comes from
+// the same merge.  No MFMA: one fma and one compare per token.
 #include <hip/hip_runtime.h>
 
 #include "walk.h"
@@ -24,7 +24,7 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
                                                                   int32_t *__restrict__ prev,
                                                                   int32_t *__restrict__ tokens) {
     extern __shared__ float lds[];
-    const int wave = threadIdx.x / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
     const int64_t b = int64_t(blockIdx.x) * HPB + wave;
     if (b >= B) return;
@@ -60,11 +60,14 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
         }
     }
 
-    const float acc = walk_into_lds(t, s, ls, ln, lane);
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
+    const float *dw = t.dense_w + size_t(h.dense_row) * V;
+    const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
     unsigned long long best = 0;
     for (int v = lane; v < V; v += kWave) {
-        const int n = ln[v];
-        const float lm = n < 0 ? acc + t.root_w[v] : ls[v];
+        float lm;
+        int n;
+        merge_slot(h, ls[v], ln[v], dw[v], dt[v], lm, n);
         const float f = __builtin_fmaf(lambda, lm, row[v]);
         if (MODE == kCtc && v == pv) continue;
         const unsigned long long k = argmax_key(f, v);
@@ -72,8 +75,10 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
     }
     const int w = argmax_index(wave_max_u64(best));
     if (lane == 0) {
-        const int n = ln[w];
-        states[b] = n < 0 ? t.root_to[w] : n;
+        float lm;
+        int n;
+        merge_slot(h, ls[w], ln[w], dw[w], dt[w], lm, n);
+        states[b] = n;
         tokens[b] = w;
         if (MODE == kCtc) prev[b] = w;
     }

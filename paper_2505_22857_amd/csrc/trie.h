@@ -3,15 +3,23 @@
 //
 // The image is one contiguous byte buffer, identical on host and device, with
 // 256-byte aligned sections (offsets in ImageHeader):
-//   rec      int4  [S]  per state {arc_begin, arc_end, backoff weight bits, backoff state}
-//                       (Section 2.2: start_arcs/end_arcs ranges, boff_weights,
-//                       boff_to_states); state 0 (empty context) has an empty range
-//   root_w   float [V]  dense row of the empty context: unigram weight, or <unk>
-//   root_to  int32 [V]  next state of each unigram arc (0 for <unk> tokens)
-//   arc_tok  int32 [A]  arcs of non-empty contexts, sorted by (from_state, token)
-//   arc_w    float [A]
-//   arc_to   int32 [A]
-//   status   int32 [4]  device-written counters ([0]: out-of-range input states)
+//   status   int32 [4]   device-written counters ([0]: out-of-range input states)
+//   chain    per state, its whole backoff chain, grouped by order k and
+//            addressed as chain + off_order[k] + (s - first[k]) * 16 * max(k, 1):
+//              ChainHead {dense_row, acc1, acc0, nlev}
+//              ChainLevel[nlev] {arc_begin, arc_end, acc}   (orders k, k-1, ..., 2)
+//            The accumulators are the fp32 left fold of the backoff weights
+//            from the query state downward (Algorithm 1), computed on the host
+//            in the same order the walk would take, so they are bit-identical
+//            to a walk that adds them one by one.
+//   dense_w  float [R * V]  dense rows: row 0 is the empty context (unigram or
+//   dense_to int32 [R * V]  <unk> weight), row u = 1..n1 is the order-1 state u:
+//            its own bigram weight and state where listed, else the
+//            empty-context entry with DENSE_BACKOFF set in dense_to (that
+//            token's score takes acc0 instead of acc1).
+//   arc_tok  int32 [A3]  arcs of states of order >= 2 (n-grams of order >= 3),
+//   arc_w    float [A3]  sorted by (from_state, token) (Section 2.2)
+//   arc_to   int32 [A3]
 #pragma once
 
 #include <cstddef>
@@ -23,33 +31,50 @@
 
 namespace ngpu {
 
-constexpr uint32_t kImageMagic = 0x4d4c504e;  // "NPLM"
+constexpr uint32_t kImageMagic = 0x324d4c4e;  // "NLM2"
 constexpr size_t kAlign = 256;
+constexpr int32_t kDenseBackoff = int32_t(0x80000000u);  // flag bit in dense_to
 
 struct ImageHeader {
     uint32_t magic;
     int32_t vocab_size;
     int32_t max_order;
-    int32_t pad0;
+    int32_t dense_rows;
     int64_t num_states;
-    int64_t num_arcs;
-    uint64_t off_rec, off_root_w, off_root_to, off_arc_tok, off_arc_w, off_arc_to, off_status;
+    int64_t num_arcs;            // sparse arcs in the image (orders >= 3)
+    uint64_t off_status, off_chain, off_dense_w, off_dense_to, off_arc_tok, off_arc_w, off_arc_to;
     uint64_t total_bytes;
+    int32_t first[NGPU_LM_MAX_ORDER + 1];       // first state id of each order; first[N] = S
+    uint64_t off_order[NGPU_LM_MAX_ORDER];      // chain offset (from the chain section) per order
 };
 
-struct StateRec {
+struct ChainHead {
+    int32_t dense_row;
+    float acc1;   // accumulator at the order-1 ancestor: applies to its own bigrams
+    float acc0;   // accumulator at the empty context: applies to backed-off tokens
+    int32_t nlev;
+};
+struct ChainLevel {
     int32_t begin;
+    int32_t end;
+    float acc;
+    int32_t pad;
+};
+static_assert(sizeof(ChainHead) == 16 && sizeof(ChainLevel) == 16, "chain records are 16-byte units");
+
+// Host-side CSR record (not in the device image): used for byte accounting.
+struct StateRec {
+    int32_t begin;  // into the host arc numbering (orders >= 2)
     int32_t end;
     float bw;
     int32_t bto;
 };
-static_assert(sizeof(StateRec) == 16, "state record must be 16 bytes");
 
 // Kernel view of an uploaded image.
 struct DevTrie {
-    const StateRec *rec;
-    const float *root_w;
-    const int32_t *root_to;
+    const unsigned char *chain;
+    const float *dense_w;
+    const int32_t *dense_to;
     const int32_t *arc_tok;
     const float *arc_w;
     const int32_t *arc_to;
@@ -57,6 +82,9 @@ struct DevTrie {
     int32_t num_states;
     int32_t vocab_size;
     int32_t max_order;
+    int32_t pad;
+    int32_t first[NGPU_LM_MAX_ORDER + 1];
+    uint64_t off_order[NGPU_LM_MAX_ORDER];
 };
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -65,18 +93,14 @@ inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct ngpu_lm {
     int32_t V = 0, N = 0;
-    int64_t S = 0, A = 0;
+    int64_t S = 0, A = 0;                 // A: arcs of orders >= 2 (host numbering)
     std::vector<unsigned char> image;     // host copy of the device image
     ngpu::ImageHeader hdr{};
-    std::vector<int64_t> state_first;     // first state id of each order 1..N-1 (index by order)
+    std::vector<ngpu::StateRec> rec;      // [S] CSR records over the host arc numbering
     std::vector<int32_t> state_parent;    // [S] state of the context minus its last token
     std::vector<int32_t> state_tok;       // [S] last token of the context
     void *dev = nullptr;                  // uploaded image (caller-owned)
     int device = -1;
-
-    const ngpu::StateRec *rec() const {
-        return reinterpret_cast<const ngpu::StateRec *>(image.data() + hdr.off_rec);
-    }
 };
 
 namespace ngpu {

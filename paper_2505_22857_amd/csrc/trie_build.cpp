@@ -7,7 +7,10 @@
 // the canonical numbering (order, tuple).  The prefix of an order-k key is
 // key >> bits and its suffix is the low (k-1)*bits bits, so the closure checks,
 // the backoff state (the suffix) and the arc ranges (children share the prefix)
-// are binary searches and scans over the sorted keys.
+// are binary searches and scans over the sorted keys.  The image then holds,
+// per state, its whole backoff chain (arc ranges and accumulators), dense rows
+// for the empty context and the order-1 states, and the sparse arcs of the
+// deeper states (layout in trie.h).
 #include <algorithm>
 #include <cmath>
 #include <cstring>
@@ -182,57 +185,8 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
         return NGPU_E_TOO_LARGE;
     }
 
-    // ---- image layout
-    ImageHeader h{};
-    h.magic = kImageMagic;
-    h.vocab_size = V;
-    h.max_order = N;
-    h.num_states = S;
-    h.num_arcs = A;
-    size_t off = align_up(sizeof(ImageHeader));
-    h.off_status = off;
-    off = align_up(off + 4 * sizeof(int32_t));
-    h.off_rec = off;
-    off = align_up(off + size_t(S) * sizeof(StateRec));
-    h.off_root_w = off;
-    off = align_up(off + size_t(V) * 4);
-    h.off_root_to = off;
-    off = align_up(off + size_t(V) * 4);
-    h.off_arc_tok = off;
-    off = align_up(off + size_t(A) * 4);
-    h.off_arc_w = off;
-    off = align_up(off + size_t(A) * 4);
-    h.off_arc_to = off;
-    off = align_up(off + size_t(A) * 4);
-    h.total_bytes = off;
-
-    std::vector<unsigned char> img;
-    try {
-        img.assign(off, 0);
-    } catch (const std::bad_alloc &) {
-        *err = "host allocation of the trie image failed";
-        return NGPU_E_NO_MEMORY;
-    }
-    std::memcpy(img.data(), &h, sizeof h);
-    StateRec *rec = reinterpret_cast<StateRec *>(img.data() + h.off_rec);
-    float *root_w = reinterpret_cast<float *>(img.data() + h.off_root_w);
-    int32_t *root_to = reinterpret_cast<int32_t *>(img.data() + h.off_root_to);
-    int32_t *arc_tok = reinterpret_cast<int32_t *>(img.data() + h.off_arc_tok);
-    float *arc_w = reinterpret_cast<float *>(img.data() + h.off_arc_w);
-    int32_t *arc_to = reinterpret_cast<int32_t *>(img.data() + h.off_arc_to);
-
-    // dense row of the empty context (Section 2.2: every token has an arc; missing ones get <unk>)
-    for (int32_t v = 0; v < V; ++v) {
-        root_w[v] = has_unk ? unk : 0.0f;
-        root_to[v] = 0;
-    }
-    for (size_t p = 0; p < lv[1].key.size(); ++p) {
-        int32_t v = int32_t(uint64_t(lv[1].key[p]));
-        root_w[v] = lv[1].w[p];
-        root_to[v] = N > 1 ? int32_t(first[1] + int64_t(p)) : 0;
-    }
-
-    // state records; state 0 has no sparse arcs (its row is dense)
+    // ---- host CSR records over the host arc numbering (orders 2..N at arc_base[k])
+    std::vector<StateRec> rec(static_cast<size_t>(S));
     rec[0] = StateRec{0, 0, 0.0f, 0};
     lm->state_parent.assign(size_t(S), 0);
     lm->state_tok.assign(size_t(S), -1);
@@ -255,14 +209,116 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
             lm->state_tok[id] = int32_t(uint64_t(L.key[p]) & tmask);
         }
     }
-    // arcs of orders 2..N: token, weight, next state
-    for (int k = 2; k <= N; ++k) {
+    const int64_t n1 = N > 1 ? int64_t(lv[1].key.size()) : 0;   // order-1 states
+    const int64_t A3 = N >= 3 ? A - int64_t(lv[2].key.size()) : 0;  // arcs of orders >= 3
+    const int64_t arc3 = N >= 3 ? arc_base[3] : 0;                  // host index of the first one
+    const int64_t R = 1 + n1;                                       // dense rows
+
+    // ---- image layout
+    ImageHeader h{};
+    h.magic = kImageMagic;
+    h.vocab_size = V;
+    h.max_order = N;
+    h.dense_rows = int32_t(R);
+    h.num_states = S;
+    h.num_arcs = A3;
+    for (int k = 0; k <= NGPU_LM_MAX_ORDER; ++k) h.first[k] = int32_t(k == 0 ? 0 : (k < N ? first[k] : S));
+    size_t off = align_up(sizeof(ImageHeader));
+    h.off_status = off;
+    off = align_up(off + 4 * sizeof(int32_t));
+    h.off_chain = off;
+    size_t coff = 0;
+    for (int k = 0; k < N; ++k) {
+        h.off_order[k] = coff;
+        const int64_t cnt = k == 0 ? 1 : (k + 1 < N ? first[k + 1] : S) - first[k];
+        coff += size_t(cnt) * 16 * size_t(k == 0 ? 1 : k);
+    }
+    off = align_up(off + coff);
+    h.off_dense_w = off;
+    off = align_up(off + size_t(R) * size_t(V) * 4);
+    h.off_dense_to = off;
+    off = align_up(off + size_t(R) * size_t(V) * 4);
+    h.off_arc_tok = off;
+    off = align_up(off + size_t(A3) * 4);
+    h.off_arc_w = off;
+    off = align_up(off + size_t(A3) * 4);
+    h.off_arc_to = off;
+    off = align_up(off + size_t(A3) * 4);
+    h.total_bytes = off;
+
+    std::vector<unsigned char> img;
+    try {
+        img.assign(off, 0);
+    } catch (const std::bad_alloc &) {
+        *err = "host allocation of the trie image failed";
+        return NGPU_E_NO_MEMORY;
+    }
+    std::memcpy(img.data(), &h, sizeof h);
+    unsigned char *chain = img.data() + h.off_chain;
+    float *dense_w = reinterpret_cast<float *>(img.data() + h.off_dense_w);
+    int32_t *dense_to = reinterpret_cast<int32_t *>(img.data() + h.off_dense_to);
+    int32_t *arc_tok = reinterpret_cast<int32_t *>(img.data() + h.off_arc_tok);
+    float *arc_w = reinterpret_cast<float *>(img.data() + h.off_arc_w);
+    int32_t *arc_to = reinterpret_cast<int32_t *>(img.data() + h.off_arc_to);
+
+    // dense row 0: the empty context (Section 2.2: every token has an arc; missing ones get <unk>)
+    for (int32_t v = 0; v < V; ++v) {
+        dense_w[v] = has_unk ? unk : 0.0f;
+        dense_to[v] = 0;
+    }
+    for (size_t p = 0; p < lv[1].key.size(); ++p) {
+        int32_t v = int32_t(uint64_t(lv[1].key[p]));
+        dense_w[v] = lv[1].w[p];
+        dense_to[v] = N > 1 ? int32_t(first[1] + int64_t(p)) : 0;
+    }
+    // dense rows of the order-1 states: own bigrams, else the empty-context entry flagged
+    for (int64_t u = 1; u <= n1; ++u) {
+        float *rw = dense_w + size_t(u) * size_t(V);
+        int32_t *rt = dense_to + size_t(u) * size_t(V);
+        for (int32_t v = 0; v < V; ++v) {
+            rw[v] = dense_w[v];
+            rt[v] = dense_to[v] | kDenseBackoff;
+        }
+        const OrderLevel &L2 = lv[2];
+        for (int32_t a = rec[u].begin; a < rec[u].end; ++a) {   // order-2 arcs: host index = rank
+            int32_t v = int32_t(uint64_t(L2.key[a]) & tmask);
+            rw[v] = L2.w[a];
+            rt[v] = N > 2 ? int32_t(first[2] + a) : int32_t(first[1] + L2.suffix[a]);
+        }
+    }
+    // sparse arcs of orders 3..N: token, weight, next state
+    for (int k = 3; k <= N; ++k) {
         const OrderLevel &L = lv[k];
         for (size_t p = 0; p < L.key.size(); ++p) {
-            int64_t a = arc_base[k] + int64_t(p);
+            int64_t a = arc_base[k] - arc3 + int64_t(p);
             arc_tok[a] = int32_t(uint64_t(L.key[p]) & tmask);
             arc_w[a] = L.w[p];
             arc_to[a] = k < N ? int32_t(first[k] + int64_t(p)) : int32_t(first[N - 1] + L.suffix[p]);
+        }
+    }
+    // chain records: the fp32 fold of backoff weights from the state downward
+    std::memset(chain, 0, 16);   // the empty context: dense row 0, accumulators 0, no sparse level
+    for (int k = 1; k < N; ++k) {
+        const int64_t end = k + 1 < N ? first[k + 1] : S;
+        for (int64_t s0 = first[k]; s0 < end; ++s0) {
+            unsigned char *r = chain + h.off_order[k] + size_t(s0 - first[k]) * 16 * size_t(k);
+            ChainLevel *lev = reinterpret_cast<ChainLevel *>(r + 16);
+            float acc = 0.0f;
+            int64_t s = s0;
+            for (int j = 0; j < k - 1; ++j) {   // states of order k, k-1, ..., 2
+                lev[j].begin = int32_t(rec[s].begin - arc3);
+                lev[j].end = int32_t(rec[s].end - arc3);
+                lev[j].acc = acc;
+                lev[j].pad = 0;
+                acc = acc + rec[s].bw;
+                s = rec[s].bto;
+            }
+            ChainHead hd;
+            hd.dense_row = int32_t(s);           // the order-1 ancestor: state id u is dense row u
+            hd.acc1 = acc;
+            hd.acc0 = acc + rec[s].bw;
+            hd.nlev = k - 1;
+            std::memcpy(r, &hd, sizeof hd);
         }
     }
 
@@ -271,7 +327,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
     lm->S = S;
     lm->A = A;
     lm->hdr = h;
-    lm->state_first.assign(first.begin(), first.end());
+    lm->rec.swap(rec);
     lm->image.swap(img);
     return NGPU_OK;
 }

@@ -1,15 +1,18 @@
 // Device-side backoff walk shared by the advance and fused-step kernels.
 //
-// One wavefront (64 lanes) owns one hypothesis and a V-wide row in LDS:
-// ln[v] = next state (-1 while no level above the empty context holds v),
-// ls[v] = score.  The walk visits the query state and its backoff states down
-// to (not including) the empty context, highest order first (Algorithm 1):
-// each level's arcs are spread over the lanes and scattered into the slots that
-// are still unset, then the level's backoff weight joins the accumulator.  The
-// dense empty-context row is merged afterwards by whoever reads the LDS row, so
-// it is never scattered.  Within a level the tokens are distinct, so lanes never
-// race on a slot; across levels the LDS operations of one wavefront complete in
-// program order, so a later level sees every slot an earlier level set.
+// One wavefront (64 lanes) owns one hypothesis.  Its state's chain record
+// (one 16-byte head plus one 16-byte entry per state of order >= 2 on the
+// backoff chain) gives every sparse level's arc range and accumulator at
+// once, so the only dependent loads are state -> chain record -> arcs.  The
+// sparse levels are scattered, highest order first (Algorithm 1), into the
+// wavefront's V-wide LDS row (ln[v] = next state or -1 while unset, ls[v] =
+// score), with all arc loads of a stripe issued before any LDS access.  The
+// order-1 ancestor's dense row, which already folds in the empty context,
+// supplies every slot left unset; it is merged by whoever reads the LDS row.
+//
+// Races: within a level the tokens are distinct, so lanes never write the same
+// slot; across levels the LDS operations of one wavefront complete in program
+// order, so a later (lower-order) level sees every slot an earlier level set.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -19,26 +22,69 @@
 namespace ngpu {
 
 constexpr int kWave = 64;
+constexpr int kArcUnroll = 4;   // arc stripes of 64 lanes loaded before the LDS scatter
 
-// Walks state s into (ls, ln); returns the accumulator at the empty context.
-__device__ __forceinline__ float walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
+// Chain record of state s (s in [0, num_states)).
+__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, int s, int &order) {
+    int k = 0, fk = 0;
+    uint64_t off = t.off_order[0];
+#pragma unroll
+    for (int j = 1; j < NGPU_LM_MAX_ORDER; ++j) {
+        if (s >= t.first[j]) {   // first[] ascends; entries past the last order equal S
+            k = j;
+            fk = t.first[j];
+            off = t.off_order[j];
+        }
+    }
+    order = k;
+    return t.chain + off + size_t(s - fk) * 16u * size_t(k > 0 ? k : 1);
+}
+
+// Scatters the sparse levels of state s into (ls, ln); returns the chain head.
+__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
     const int V = t.vocab_size;
+    int order;
+    const unsigned char *rp = chain_record(t, s, order);
+    const ChainHead head = *reinterpret_cast<const ChainHead *>(rp);
+    const ChainLevel *lev = reinterpret_cast<const ChainLevel *>(rp + sizeof(ChainHead));
     for (int v = lane; v < V; v += kWave) ln[v] = -1;
-    float acc = 0.0f;
-    // a state of order k reaches the empty context after k backoffs (k < N)
-    for (int lvl = 0; lvl < t.max_order && s != 0; ++lvl) {
-        const StateRec r = t.rec[s];
-        for (int a = r.begin + lane; a < r.end; a += kWave) {
-            const int tok = t.arc_tok[a];
-            if (ln[tok] < 0) {
-                ls[tok] = acc + t.arc_w[a];
-                ln[tok] = t.arc_to[a];
+    for (int j = 0; j < head.nlev; ++j) {
+        const ChainLevel L = lev[j];
+        for (int a0 = L.begin; a0 < L.end; a0 += kWave * kArcUnroll) {
+            int tok[kArcUnroll], to[kArcUnroll];
+            float w[kArcUnroll];
+#pragma unroll
+            for (int u = 0; u < kArcUnroll; ++u) {
+                const int a = a0 + u * kWave + lane;
+                tok[u] = -1;
+                if (a < L.end) {
+                    tok[u] = t.arc_tok[a];
+                    w[u] = t.arc_w[a];
+                    to[u] = t.arc_to[a];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kArcUnroll; ++u) {
+                if (tok[u] >= 0 && ln[tok[u]] < 0) {
+                    ls[tok[u]] = L.acc + w[u];
+                    ln[tok[u]] = to[u];
+                }
             }
         }
-        acc = acc + r.bw;
-        s = r.bto;
     }
-    return acc;
+    return head;
+}
+
+// Final value of one token: the LDS slot if a sparse level set it, else the
+// dense row entry with the accumulator its flag selects.
+__device__ __forceinline__ void merge_slot(const ChainHead &h, float lsv, int lnv, float dw, int dt, float &x, int &n) {
+    if (lnv >= 0) {
+        x = lsv;
+        n = lnv;
+    } else {
+        x = ((dt & kDenseBackoff) ? h.acc0 : h.acc1) + dw;
+        n = dt & 0x7fffffff;
+    }
 }
 
 // Wave-wide maximum of a 64-bit key.

@@ -40,35 +40,53 @@ def test_library_exports_every_declared_symbol(lib):
     assert sorted(ng.EXPORTED) == decl
 
 
+HDR_FMT = "<IiiiqqQQQQQQQQ11i4x10Q"
+
+
 def parse_image(img):
-    hdr = struct.unpack_from("<IiiiqqQQQQQQQQ", img.tobytes()[:128])
-    magic, V, N, _, S, A, o_rec, o_rw, o_rt, o_tok, o_w, o_to, o_st, total = hdr
-    assert magic == 0x4D4C504E and total == len(img)
-    rec = np.frombuffer(img, np.int32, 4 * S, o_rec).reshape(S, 4)
-    return dict(V=V, N=N, S=S, A=A,
-                begin=rec[:, 0], end=rec[:, 1], bw=rec[:, 2].view(np.float32), bto=rec[:, 3],
-                root_w=np.frombuffer(img, np.float32, V, o_rw), root_to=np.frombuffer(img, np.int32, V, o_rt),
-                tok=np.frombuffer(img, np.int32, A, o_tok), w=np.frombuffer(img, np.float32, A, o_w),
-                to=np.frombuffer(img, np.int32, A, o_to))
+    """White-box view of the image (layout of csrc/trie.h)."""
+    raw = img.tobytes()
+    f = struct.unpack_from(HDR_FMT, raw)
+    magic, V, N, R, S, A3 = f[:6]
+    o_st, o_ch, o_dw, o_dt, o_tok, o_w, o_to, total = f[6:14]
+    first = list(f[14:25])
+    off_order = list(f[25:35])
+    assert magic == 0x324D4C4E and total == len(img)
+    return dict(V=V, N=N, R=R, S=S, A=A3, first=first, off_order=off_order, raw=raw, o_ch=o_ch,
+                dense_w=np.frombuffer(raw, np.float32, R * V, o_dw).reshape(R, V),
+                dense_to=np.frombuffer(raw, np.int32, R * V, o_dt).reshape(R, V),
+                tok=np.frombuffer(raw, np.int32, A3, o_tok), w=np.frombuffer(raw, np.float32, A3, o_w),
+                to=np.frombuffer(raw, np.int32, A3, o_to))
+
+
+def chain_of(im, s):
+    k = 0
+    for j in range(1, 10):
+        if s >= im["first"][j]:
+            k = j
+    off = im["o_ch"] + im["off_order"][k] + (s - im["first"][k]) * 16 * max(k, 1)
+    row, acc1, acc0, nlev = struct.unpack_from("<iffi", im["raw"], off)
+    levels = [struct.unpack_from("<iif", im["raw"], off + 16 * (j + 1)) for j in range(nlev)]
+    return k, row, np.float32(acc1), np.float32(acc0), levels
 
 
 def walk_image(im, s):
-    """Algorithm 1 over the image arrays, in fp32."""
+    """The query over the image arrays on the CPU: sparse levels, then the dense row."""
     V = im["V"]
     nxt = np.full(V, -1, np.int32)
     sc = np.zeros(V, np.float32)
-    acc = np.float32(0.0)
-    while s != 0:
-        b, e = im["begin"][s], im["end"][s]
+    k, row, acc1, acc0, levels = chain_of(im, s)
+    for b, e, acc in levels:
         toks = im["tok"][b:e]
         unset = nxt[toks] == -1
-        sc[toks[unset]] = acc + im["w"][b:e][unset]
+        sc[toks[unset]] = np.float32(acc) + im["w"][b:e][unset]
         nxt[toks[unset]] = im["to"][b:e][unset]
-        acc = np.float32(acc + im["bw"][s])
-        s = im["bto"][s]
     unset = nxt == -1
-    sc[unset] = acc + im["root_w"][unset]
-    nxt[unset] = im["root_to"][unset]
+    dt = im["dense_to"][row]
+    flag = dt < 0
+    acc = np.where(flag, acc0, acc1).astype(np.float32)
+    sc[unset] = (acc + im["dense_w"][row])[unset]
+    nxt[unset] = (dt & 0x7FFFFFFF)[unset]
     return sc, nxt
 
 
@@ -112,22 +130,32 @@ def test_numbering_matches_oracle_on_shuffled_lists():
             assert lm.state_context(int(s)) == o.state_context(int(s))
 
 
-def test_csr_rows_sorted_and_consistent():
+def test_chain_records_and_sparse_rows():
     m = make_config_model(2)
     lm = ng.NgpuLM.from_model(m)
+    o = Oracle.from_model(m)
     im = parse_image(lm.host_image())
-    b, e = im["begin"], im["end"]
-    assert b[0] == e[0] == 0
-    assert (e >= b).all() and (b[1:] >= 0).all() and (e <= im["A"]).all()
-    # one contiguous range per state, in state order, covering every arc
-    assert b[1] == 0 and (b[2:] == e[1:-1]).all() and e[-1] == im["A"]
-    for s in np.random.default_rng(1).integers(1, im["S"], 500):
-        t = im["tok"][b[s]:e[s]]
-        assert (np.diff(t) > 0).all()
-    # arcs of orders below N lead to the arc's own state, i.e. id = arc index + a constant
-    n_low = sum(m.counts[1:-1])
-    to = im["to"][:n_low]
-    assert (np.diff(to) == 1).all()
+    order, tokens, W, B = m.to_list()
+    Bd = {tuple(t[:k]): b for k, t, b in zip(order, tokens, B)}
+    assert im["R"] == 1 + m.counts[0]
+    for s in np.random.default_rng(1).integers(1, im["S"], 400):
+        ctx = o.state_context(int(s))
+        k, row, acc1, acc0, levels = chain_of(im, int(s))
+        assert k == len(ctx) and len(levels) == k - 1
+        # dense row = the order-1 ancestor (the context's last token); accumulators are the fp32 fold
+        assert row == o.state_of(ctx[-1:])
+        acc = np.float32(0.0)
+        for j, (b, e, a) in enumerate(levels):
+            assert np.float32(a) == acc
+            t = im["tok"][b:e]
+            assert (np.diff(t) > 0).all() and (b <= e)
+            acc = np.float32(acc + np.float32(Bd[ctx[j:]]))
+        assert acc1 == acc and acc0 == np.float32(acc + np.float32(Bd[ctx[-1:]]))
+    # the dense row of an order-1 state flags exactly the tokens it does not continue with
+    u = 5
+    flagged = im["dense_to"][u] < 0
+    own = {int(t[1]) for k, t in zip(order, tokens) if k == 2 and t[0] == u - 1}
+    assert set(np.nonzero(~flagged)[0].tolist()) == own
 
 
 def _raw_build(V, N, order, tokens, W, B, unk=float("nan"), flags=0):
@@ -188,18 +216,17 @@ def test_queries_before_upload_fail_cleanly():
 
 
 def test_query_bytes():
-    m = make_config_model(1)
+    m = make_config_model(2)
     lm = ng.NgpuLM.from_model(m)
     V = m.vocab_size
     hbm, tot = lm.query_bytes(np.zeros(3, np.int32))
-    assert hbm == 3 * 8 * V and tot == 3 * 16 * V
+    assert hbm == 3 * (8 * V + 16) and tot == hbm + 3 * 8 * V
     im = parse_image(lm.host_image())
-    s = m.state_offset(2) + 5                      # an order-2 state: its record and arcs are HBM traffic
-    deg2 = im["end"][s] - im["begin"][s]
-    s1 = im["bto"][s]
-    deg1 = im["end"][s1] - im["begin"][s1]
+    s = m.state_offset(3) + 5                      # an order-3 state: two sparse levels
+    k, row, acc1, acc0, levels = chain_of(im, s)
+    arcs = sum(e - b for b, e, _ in levels)
     hbm, tot = lm.query_bytes(np.array([s], np.int32))
-    assert hbm == 8 * V + 16 + 12 * deg2
-    assert tot == hbm + 8 * V + 16 + 12 * deg1
+    assert hbm == 8 * V + 16 * 3 + 12 * arcs
+    assert tot == hbm + 8 * V
     with pytest.raises(ng.NgpuError):
         lm.query_bytes(np.array([m.num_states], np.int32))

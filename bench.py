@@ -74,7 +74,8 @@ def main():
     ap.add_argument("--fused-frames", type=int, default=1000)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time; 0 skips")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run a plain 512 MiB device copy (for counter calibration)")
+                    help="also run a plain 512 MiB device copy and fill (counter calibration)")
+    ap.add_argument("--advance-only", action="store_true", help="skip the fused step and the oracle")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
@@ -109,12 +110,25 @@ def main():
     stream = torch.cuda.current_stream()
 
     if args.copy_calibration:
+        # reference kernels of known traffic: a 512 MiB device copy and a 512 MiB fill
         src = torch.empty(2**29 // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        dst.copy_(src)
+        c0.record(stream)
         for _ in range(5):
             dst.copy_(src)
+        c1.record(stream)
         torch.cuda.synchronize()
-        log("copy calibration: 5 copies of 512 MiB")
+        cp_ms = c0.elapsed_time(c1) / 5
+        c0.record(stream)
+        for _ in range(5):
+            dst.fill_(2.0)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        fill_ms = c0.elapsed_time(c1) / 5
+        log(f"reference: 512 MiB copy {cp_ms:.3f} ms ({2 * 2**29 / cp_ms / 1e6:.0f} GB/s read+write), "
+            f"512 MiB fill {fill_ms:.3f} ms ({2**29 / fill_ms / 1e6:.0f} GB/s)")
         del src, dst
 
     # ---- single 512-hypothesis call latency
@@ -156,6 +170,9 @@ def main():
     log(f"advance B={B}: wall {ms_per_step:.3f} ms/step, kernel mean {mean_ms:.3f} ms "
         f"(min {kern_ms.min():.3f}), {achieved:.0f} GB/s algorithmic HBM, "
         f"{total_bytes / (mean_ms * 1e-3) / 1e9:.0f} GB/s incl. cache-resident rows")
+
+    if args.advance_only:
+        return
 
     # ---- fused greedy CTC step (the config-5 shape), per frame
     fspec = CONFIGS[5]

@@ -1,12 +1,20 @@
 // Batched full-vocabulary backoff query (Algorithm 1, batched over hypotheses).
 //
-// Grid: one wavefront per hypothesis, HPB wavefronts per workgroup, each with
-// its own V-wide score/state row in LDS (8 bytes per token).  After the
-// sparse levels are scattered, the row is merged with the order-1 ancestor's
-// dense row and written to HBM with 16-byte stores (when V is a multiple of
-// 4): lane l covers tokens 4l..4l+3 of each 256-token stripe, so one store
-// instruction of the wavefront writes 1 KiB contiguously.  No MFMA: the work
-// is gathers, scatters and one fp32 add per token.
+// One wavefront per hypothesis, HPB wavefronts per workgroup, each with its
+// own V-wide score/state row in LDS (8 bytes per token).  After the sparse
+// levels are scattered, the row is merged with the order-1 ancestor's dense
+// row and written to HBM with 16-byte stores (when V is a multiple of 4):
+// lane l covers tokens 4l..4l+3 of each 256-token stripe, so one store
+// instruction of the wavefront writes 1 KiB contiguously.
+//
+// XCD-aware distribution (G = 8): workgroups are dispatched round-robin over
+// the eight XCDs, so workgroup i serves dense-row group i % 8.  Each wavefront
+// scans G consecutive hypotheses (lane i loads the state and chain head of
+// hypothesis i, two vector loads) and processes the ones whose dense row lies
+// in its group; the eight workgroups of a chunk together cover every
+// hypothesis exactly once.  Each XCD's L2 then holds an eighth of the dense
+// rows instead of all of them.  G = 1 is the plain one-hypothesis-per-wave
+// mapping.  No MFMA: the work is gathers, scatters and one fp32 add per token.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -15,71 +23,102 @@
 
 namespace ngpu {
 
-template <int HPB, bool VEC>
+template <int HPB, bool VEC, int G>
 __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const int32_t *__restrict__ states,
                                                                int64_t B, float *__restrict__ scores,
                                                                int32_t *__restrict__ next) {
     extern __shared__ float lds[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
-    const int64_t b = int64_t(blockIdx.x) * HPB + wave;
-    if (b >= B) return;  // whole wavefronts leave; no workgroup barrier is used
+    const int grp = int(blockIdx.x % G);
+    const int64_t base = (int64_t(blockIdx.x / G) * HPB + wave) * G;
+    if (base >= B) return;  // whole wavefronts leave; no workgroup barrier is used
     const int V = t.vocab_size;
     float *ls = lds + size_t(wave) * 2 * V;
     int *ln = reinterpret_cast<int *>(ls + V);
-    float *orow = scores + b * V;
-    int32_t *nrow = next + b * V;
 
-    const int s = __builtin_amdgcn_readfirstlane(states[b]);
-    if (s < 0 || s >= t.num_states) {
-        if (lane == 0) atomicAdd(&t.status[0], 1);
-        for (int v = lane; v < V; v += kWave) {
-            orow[v] = NAN;
-            nrow[v] = -1;
+    // scan: lane i < G looks at hypothesis base + i
+    int s_l = -1;
+    int4 head_l = make_int4(0, 0, 0, 0);
+    uint64_t rp_l = 0;
+    bool mine = false;
+    const int64_t bl = base + lane;
+    if (lane < G && bl < B) {
+        s_l = states[bl];
+        if (s_l < 0 || s_l >= t.num_states) {
+            s_l = -1;
+            mine = (bl % G) == grp;   // an invalid state's row is written by one owner
+        } else {
+            const unsigned char *rp = chain_record(t, s_l);
+            rp_l = reinterpret_cast<uint64_t>(rp);
+            head_l = *reinterpret_cast<const int4 *>(rp);
+            mine = (head_l.w >> 16) == grp;
         }
-        return;
     }
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
-    const float *dw = t.dense_w + size_t(h.dense_row) * V;
-    const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
-
-    if (VEC) {
-        for (int v = lane * 4; v < V; v += 4 * kWave) {
-            const int4 n4 = *reinterpret_cast<const int4 *>(ln + v);
-            const float4 x4 = *reinterpret_cast<const float4 *>(ls + v);
-            const float4 w4 = *reinterpret_cast<const float4 *>(dw + v);
-            const int4 t4 = *reinterpret_cast<const int4 *>(dt + v);
-            float4 xo;
-            int4 no;
-            merge_slot(h, x4.x, n4.x, w4.x, t4.x, xo.x, no.x);
-            merge_slot(h, x4.y, n4.y, w4.y, t4.y, xo.y, no.y);
-            merge_slot(h, x4.z, n4.z, w4.z, t4.z, xo.z, no.z);
-            merge_slot(h, x4.w, n4.w, w4.w, t4.w, xo.w, no.w);
-            *reinterpret_cast<float4 *>(orow + v) = xo;
-            *reinterpret_cast<int4 *>(nrow + v) = no;
+    uint64_t todo = __ballot(mine);
+    while (todo) {
+        const int i = __builtin_ctzll(todo);
+        todo &= todo - 1;
+        const int64_t b = base + i;
+        float *orow = scores + b * V;
+        int32_t *nrow = next + b * V;
+        const int s = __builtin_amdgcn_readlane(s_l, i);
+        if (s < 0) {
+            if (lane == 0) atomicAdd(&t.status[0], 1);
+            for (int v = lane; v < V; v += kWave) {
+                orow[v] = NAN;
+                nrow[v] = -1;
+            }
+            continue;
         }
-    } else {
-        for (int v = lane; v < V; v += kWave) {
-            float x;
-            int n;
-            merge_slot(h, ls[v], ln[v], dw[v], dt[v], x, n);
-            orow[v] = x;
-            nrow[v] = n;
+        ChainHead h;
+        h.dense_row = __builtin_amdgcn_readlane(head_l.x, i);
+        h.acc1 = __int_as_float(__builtin_amdgcn_readlane(head_l.y, i));
+        h.acc0 = __int_as_float(__builtin_amdgcn_readlane(head_l.z, i));
+        h.nlev_group = __builtin_amdgcn_readlane(head_l.w, i);
+        const uint64_t rpu = (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(rp_l >> 32), i))) << 32) |
+                             uint32_t(__builtin_amdgcn_readlane(int(rp_l & 0xffffffffu), i));
+        scatter_levels(t, reinterpret_cast<const unsigned char *>(rpu), chain_levels(h), ls, ln, lane);
+        const float *dw = t.dense_w + size_t(h.dense_row) * V;
+        const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
+
+        if (VEC) {
+            for (int v = lane * 4; v < V; v += 4 * kWave) {
+                const int4 n4 = *reinterpret_cast<const int4 *>(ln + v);
+                const float4 x4 = *reinterpret_cast<const float4 *>(ls + v);
+                const float4 w4 = *reinterpret_cast<const float4 *>(dw + v);
+                const int4 t4 = *reinterpret_cast<const int4 *>(dt + v);
+                float4 xo;
+                int4 no;
+                merge_slot(h, x4.x, n4.x, w4.x, t4.x, xo.x, no.x);
+                merge_slot(h, x4.y, n4.y, w4.y, t4.y, xo.y, no.y);
+                merge_slot(h, x4.z, n4.z, w4.z, t4.z, xo.z, no.z);
+                merge_slot(h, x4.w, n4.w, w4.w, t4.w, xo.w, no.w);
+                *reinterpret_cast<float4 *>(orow + v) = xo;
+                *reinterpret_cast<int4 *>(nrow + v) = no;
+            }
+        } else {
+            for (int v = lane; v < V; v += kWave) {
+                float x;
+                int n;
+                merge_slot(h, ls[v], ln[v], dw[v], dt[v], x, n);
+                orow[v] = x;
+                nrow[v] = n;
+            }
         }
     }
 }
 
-template <int HPB>
+template <int HPB, int G>
 static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B, float *scores,
                              int32_t *next, hipStream_t stream, bool vec) {
-    const int64_t blocks = (B + HPB - 1) / HPB;
+    const int64_t chunks = (B + int64_t(HPB) * G - 1) / (int64_t(HPB) * G);
+    const dim3 grid(unsigned(chunks * G)), block(HPB * kWave);
     const size_t lds = size_t(HPB) * 2 * size_t(t.vocab_size) * sizeof(float);
     if (vec)
-        hipLaunchKernelGGL((advance_kernel<HPB, true>), dim3(unsigned(blocks)), dim3(HPB * kWave), lds, stream,
-                           t, states, B, scores, next);
+        hipLaunchKernelGGL((advance_kernel<HPB, true, G>), grid, block, lds, stream, t, states, B, scores, next);
     else
-        hipLaunchKernelGGL((advance_kernel<HPB, false>), dim3(unsigned(blocks)), dim3(HPB * kWave), lds, stream,
-                           t, states, B, scores, next);
+        hipLaunchKernelGGL((advance_kernel<HPB, false, G>), grid, block, lds, stream, t, states, B, scores, next);
     return hipGetLastError();
 }
 
@@ -96,9 +135,9 @@ hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, fl
     const bool vec = (t.vocab_size % 4 == 0) && (reinterpret_cast<uintptr_t>(scores) % 16 == 0) &&
                      (reinterpret_cast<uintptr_t>(next) % 16 == 0);
     switch (advance_rows_per_block(t.vocab_size)) {
-        case 4: return launch_hpb<4>(t, states, B, scores, next, stream, vec);
-        case 2: return launch_hpb<2>(t, states, B, scores, next, stream, vec);
-        default: return launch_hpb<1>(t, states, B, scores, next, stream, vec);
+        case 4: return launch_hpb<4, kGroups>(t, states, B, scores, next, stream, vec);
+        case 2: return launch_hpb<2, kGroups>(t, states, B, scores, next, stream, vec);
+        default: return launch_hpb<1, kGroups>(t, states, B, scores, next, stream, vec);
     }
 }
 

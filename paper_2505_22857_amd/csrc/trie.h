@@ -6,7 +6,7 @@
 //   status   int32 [4]   device-written counters ([0]: out-of-range input states)
 //   chain    per state, its whole backoff chain, grouped by order k and
 //            addressed as chain + off_order[k] + (s - first[k]) * 16 * max(k, 1):
-//              ChainHead {dense_row, acc1, acc0, nlev}
+//              ChainHead {dense_row, acc1, acc0, nlev | group << 16}
 //              ChainLevel[nlev] {arc_begin, arc_end, acc}   (orders k, k-1, ..., 2)
 //            The accumulators are the fp32 left fold of the backoff weights
 //            from the query state downward (Algorithm 1), computed on the host
@@ -16,7 +16,10 @@
 //   dense_to int32 [R * V]  <unk> weight), row u = 1..n1 is the order-1 state u:
 //            its own bigram weight and state where listed, else the
 //            empty-context entry with DENSE_BACKOFF set in dense_to (that
-//            token's score takes acc0 instead of acc1).
+//            token's score takes acc0 instead of acc1).  Each dense row belongs
+//            to one of kGroups groups, balanced by the number of states whose
+//            chain ends in it; a query kernel may serve each group from one XCD
+//            so that the group's rows stay in that XCD's L2.
 //   arc_tok  int32 [A3]  arcs of states of order >= 2 (n-grams of order >= 3),
 //   arc_w    float [A3]  sorted by (from_state, token) (Section 2.2)
 //   arc_to   int32 [A3]
@@ -34,6 +37,7 @@ namespace ngpu {
 constexpr uint32_t kImageMagic = 0x324d4c4e;  // "NLM2"
 constexpr size_t kAlign = 256;
 constexpr int32_t kDenseBackoff = int32_t(0x80000000u);  // flag bit in dense_to
+constexpr int kGroups = 8;                                // dense-row groups (one per XCD)
 
 struct ImageHeader {
     uint32_t magic;
@@ -52,7 +56,7 @@ struct ChainHead {
     int32_t dense_row;
     float acc1;   // accumulator at the order-1 ancestor: applies to its own bigrams
     float acc0;   // accumulator at the empty context: applies to backed-off tokens
-    int32_t nlev;
+    int32_t nlev_group;   // number of sparse levels | dense-row group << 16
 };
 struct ChainLevel {
     int32_t begin;

@@ -296,8 +296,39 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
             arc_to[a] = k < N ? int32_t(first[k] + int64_t(p)) : int32_t(first[N - 1] + L.suffix[p]);
         }
     }
+    // dense-row groups: longest-processing-time assignment of rows, weighted by
+    // the number of states whose chain ends in the row, to kGroups bins
+    std::vector<int64_t> row_weight(size_t(R), 0);
+    row_weight[0] = 1;
+    for (int k = 1; k < N; ++k) {
+        const int64_t end = k + 1 < N ? first[k + 1] : S;
+        for (int64_t s0 = first[k]; s0 < end; ++s0) {
+            int64_t s = s0;
+            for (int j = 0; j < k - 1; ++j) s = rec[s].bto;
+            ++row_weight[size_t(s)];
+        }
+    }
+    std::vector<int32_t> row_group(size_t(R), 0);
+    {
+        std::vector<int64_t> order(static_cast<size_t>(R));
+        std::iota(order.begin(), order.end(), int64_t(0));
+        std::stable_sort(order.begin(), order.end(),
+                         [&](int64_t a, int64_t b) { return row_weight[a] > row_weight[b]; });
+        int64_t load[kGroups] = {0};
+        for (int64_t r : order) {
+            int g = 0;
+            for (int i = 1; i < kGroups; ++i)
+                if (load[i] < load[g]) g = i;
+            row_group[size_t(r)] = g;
+            load[g] += row_weight[size_t(r)];
+        }
+    }
+
     // chain records: the fp32 fold of backoff weights from the state downward
-    std::memset(chain, 0, 16);   // the empty context: dense row 0, accumulators 0, no sparse level
+    {
+        ChainHead root{0, 0.0f, 0.0f, row_group[0] << 16};   // the empty context: dense row 0, no sparse level
+        std::memcpy(chain, &root, sizeof root);
+    }
     for (int k = 1; k < N; ++k) {
         const int64_t end = k + 1 < N ? first[k + 1] : S;
         for (int64_t s0 = first[k]; s0 < end; ++s0) {
@@ -317,7 +348,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
             hd.dense_row = int32_t(s);           // the order-1 ancestor: state id u is dense row u
             hd.acc1 = acc;
             hd.acc0 = acc + rec[s].bw;
-            hd.nlev = k - 1;
+            hd.nlev_group = (k - 1) | (row_group[size_t(s)] << 16);
             std::memcpy(r, &hd, sizeof hd);
         }
     }

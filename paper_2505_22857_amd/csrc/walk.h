@@ -24,8 +24,8 @@ namespace ngpu {
 constexpr int kWave = 64;
 constexpr int kArcUnroll = 4;   // arc stripes of 64 lanes loaded before the LDS scatter
 
-// Chain record of state s (s in [0, num_states)).
-__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, int s, int &order) {
+// Chain record of state s (s in [0, num_states)); per-lane or uniform.
+__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, int s) {
     int k = 0, fk = 0;
     uint64_t off = t.off_order[0];
 #pragma unroll
@@ -36,19 +36,19 @@ __device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, i
             off = t.off_order[j];
         }
     }
-    order = k;
     return t.chain + off + size_t(s - fk) * 16u * size_t(k > 0 ? k : 1);
 }
 
-// Scatters the sparse levels of state s into (ls, ln); returns the chain head.
-__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
+__device__ __forceinline__ int chain_levels(const ChainHead &h) { return h.nlev_group & 0xffff; }
+__device__ __forceinline__ int chain_group(const ChainHead &h) { return h.nlev_group >> 16; }
+
+// Scatters the sparse levels of a chain record (uniform rp) into (ls, ln).
+__device__ __forceinline__ void scatter_levels(const DevTrie &t, const unsigned char *rp, int nlev, float *ls,
+                                               int *ln, int lane) {
     const int V = t.vocab_size;
-    int order;
-    const unsigned char *rp = chain_record(t, s, order);
-    const ChainHead head = *reinterpret_cast<const ChainHead *>(rp);
     const ChainLevel *lev = reinterpret_cast<const ChainLevel *>(rp + sizeof(ChainHead));
     for (int v = lane; v < V; v += kWave) ln[v] = -1;
-    for (int j = 0; j < head.nlev; ++j) {
+    for (int j = 0; j < nlev; ++j) {
         const ChainLevel L = lev[j];
         for (int a0 = L.begin; a0 < L.end; a0 += kWave * kArcUnroll) {
             int tok[kArcUnroll], to[kArcUnroll];
@@ -72,6 +72,13 @@ __device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, floa
             }
         }
     }
+}
+
+// Walks uniform state s into (ls, ln); returns the chain head.
+__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
+    const unsigned char *rp = chain_record(t, s);
+    const ChainHead head = *reinterpret_cast<const ChainHead *>(rp);
+    scatter_levels(t, rp, chain_levels(head), ls, ln, lane);
     return head;
 }
 

@@ -65,7 +65,8 @@ def chain_of(im, s):
         if s >= im["first"][j]:
             k = j
     off = im["o_ch"] + im["off_order"][k] + (s - im["first"][k]) * 16 * max(k, 1)
-    row, acc1, acc0, nlev = struct.unpack_from("<iffi", im["raw"], off)
+    row, acc1, acc0, nlev_group = struct.unpack_from("<iffi", im["raw"], off)
+    nlev = nlev_group & 0xFFFF
     levels = [struct.unpack_from("<iif", im["raw"], off + 16 * (j + 1)) for j in range(nlev)]
     return k, row, np.float32(acc1), np.float32(acc0), levels
 

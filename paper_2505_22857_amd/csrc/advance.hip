@@ -23,6 +23,9 @@
 
 namespace ngpu {
 
+typedef float nf4 __attribute__((ext_vector_type(4)));
+typedef int ni4 __attribute__((ext_vector_type(4)));
+
 template <int HPB, bool VEC, int G>
 __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const int32_t *__restrict__ states,
                                                                int64_t B, float *__restrict__ scores,
@@ -52,7 +55,7 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
             const unsigned char *rp = chain_record(t, s_l);
             rp_l = reinterpret_cast<uint64_t>(rp);
             head_l = *reinterpret_cast<const int4 *>(rp);
-            mine = (head_l.w >> 16) == grp;
+            mine = G == 1 || (head_l.w >> 16) == grp;
         }
     }
     uint64_t todo = __ballot(mine);
@@ -94,16 +97,18 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
                 merge_slot(h, x4.y, n4.y, w4.y, t4.y, xo.y, no.y);
                 merge_slot(h, x4.z, n4.z, w4.z, t4.z, xo.z, no.z);
                 merge_slot(h, x4.w, n4.w, w4.w, t4.w, xo.w, no.w);
-                *reinterpret_cast<float4 *>(orow + v) = xo;
-                *reinterpret_cast<int4 *>(nrow + v) = no;
+                // streaming stores: the rows are not read again here, so they
+                // should not displace the dense rows and arcs from the L2
+                __builtin_nontemporal_store(nf4{xo.x, xo.y, xo.z, xo.w}, reinterpret_cast<nf4 *>(orow + v));
+                __builtin_nontemporal_store(ni4{no.x, no.y, no.z, no.w}, reinterpret_cast<ni4 *>(nrow + v));
             }
         } else {
             for (int v = lane; v < V; v += kWave) {
                 float x;
                 int n;
                 merge_slot(h, ls[v], ln[v], dw[v], dt[v], x, n);
-                orow[v] = x;
-                nrow[v] = n;
+                __builtin_nontemporal_store(x, orow + v);
+                __builtin_nontemporal_store(n, nrow + v);
             }
         }
     }
@@ -122,22 +127,35 @@ static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B,
     return hipGetLastError();
 }
 
-// Wavefronts per workgroup: as many rows as fit in 32 KiB of LDS, at most 4.
-int advance_rows_per_block(int V) {
+// Launch shapes, from a sweep on the 20M n-gram workload (V = 1024):
+//  - XCD-grouped mapping from 32768 hypotheses on; below that the grouped
+//    scan costs more latency than the cache locality saves.
+//  - One wavefront per workgroup in the grouped mapping: a wavefront that finds
+//    no hypothesis of its group frees its slot (and LDS) at once instead of
+//    waiting for busier wavefronts of its workgroup.
+//  - Two wavefronts per workgroup in the plain mapping.
+constexpr int64_t kGroupedMinBatch = 32768;
+constexpr int kHpbGrouped = 1;
+constexpr int kHpbPlain = 2;
+
+// Wavefronts per workgroup: at most `want`, as many rows as fit in 32 KiB of LDS.
+int rows_per_block(int V, int want) {
     const size_t row = size_t(V) * 8;
-    if (4 * row <= 32768) return 4;
-    if (2 * row <= 32768) return 2;
-    return 1;
+    int h = want;
+    while (h > 1 && size_t(h) * row > 32768) h /= 2;
+    return h;
 }
+
+int advance_rows_per_block(int V) { return rows_per_block(V, 4); }
 
 hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, float *scores, int32_t *next,
                           hipStream_t stream) {
     const bool vec = (t.vocab_size % 4 == 0) && (reinterpret_cast<uintptr_t>(scores) % 16 == 0) &&
                      (reinterpret_cast<uintptr_t>(next) % 16 == 0);
-    switch (advance_rows_per_block(t.vocab_size)) {
-        case 4: return launch_hpb<4, kGroups>(t, states, B, scores, next, stream, vec);
-        case 2: return launch_hpb<2, kGroups>(t, states, B, scores, next, stream, vec);
-        default: return launch_hpb<1, kGroups>(t, states, B, scores, next, stream, vec);
+    if (B >= kGroupedMinBatch) return launch_hpb<kHpbGrouped, kGroups>(t, states, B, scores, next, stream, vec);
+    switch (rows_per_block(t.vocab_size, kHpbPlain)) {
+        case 2: return launch_hpb<2, 1>(t, states, B, scores, next, stream, vec);
+        default: return launch_hpb<1, 1>(t, states, B, scores, next, stream, vec);
     }
 }
 

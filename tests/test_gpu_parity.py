@@ -126,6 +126,29 @@ def test_advance_cfg4_bench_launch_sampled(dev):
     assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
 
 
+@pytest.mark.parametrize("which", ["cfg2", "V1025"])
+def test_advance_grouped_mapping_with_bad_states(dev, which):
+    """Batches of 32768 and more take the XCD-grouped mapping: every row, including
+    rows of out-of-range states (written by exactly one owner), vs the oracle."""
+    if which == "cfg2":
+        m, lm, o = cfg_pair(2)
+        B = 40000
+    else:
+        m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
+        B = 33001
+    states = uniform_states(m, B, seed=23)
+    bad = np.random.default_rng(24).choice(B, 37, replace=False)
+    states[bad[:20]] = -5
+    states[bad[20:]] = m.num_states + np.arange(17)
+    case(f"advance grouped {which} B={B} with {len(bad)} bad states")
+    sc, nx = run_advance(lm, states, dev)
+    assert lm.check_states() == len(bad)
+    good = np.setdiff1d(np.arange(B), bad)
+    assert np.isnan(sc[bad]).all() and (nx[bad] == -1).all()
+    o_s32, o_nx, _ = o.advance(states[good], nthreads=NTHREADS)
+    assert_rows(f"grouped {which}", sc[good], nx[good], o_s32, o_nx)
+
+
 @pytest.mark.parametrize("V,N", [(5, 3), (1000, 3), (1025, 4), (4096, 3), (16, 10)])
 def test_advance_odd_shapes(dev, V, N):
     if N == 10:

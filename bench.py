@@ -13,7 +13,8 @@ second over the timed steps.  The same run also reports:
   ``traffic`` is the measured HBM bytes per launch from the committed rocprofv3
   counter summary when it was taken on the current kernel source, else null;
 * latency of a single 512-hypothesis call (median of 100);
-* the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame;
+* the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame,
+  and the same decode of 1000 frames as one launch;
 * cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
   host cores.
 """
@@ -204,7 +205,32 @@ def main():
              "steps_per_s": T / (f_ms * 1e-3), "frames_per_s": Bf * T / (f_ms * 1e-3),
              "us_per_step": f_ms * 1e3 / T}
     log(f"fused CTC: {fused['us_per_step']:.1f} us/step, {fused['frames_per_s']:.3g} frames/s")
-    del asr
+
+    # ---- the same decode as one launch over all frames
+    asr_bt = asr.permute(1, 0, 2)            # [B, T, C] view, unit class stride
+    labels = torch.empty((Bf, T), dtype=torch.int32, device=dev)
+    fst.zero_()
+    prev.fill_(V)
+    lm.fused_greedy_decode(asr_bt, fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, labels=labels)
+    torch.cuda.synchronize()
+    d_ms = []
+    for _ in range(3):
+        fst.zero_()
+        prev.fill_(V)
+        f0.record(stream)
+        lm.fused_greedy_decode(asr_bt, fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, labels=labels)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        d_ms.append(f0.elapsed_time(f1))
+    assert lm.check_states() == 0
+    dm = float(np.median(d_ms))
+    fused_decode = {"workload": f"CTC, B={Bf} utterances x {T} frames, {V + 1} classes, lambda={fspec.lam}, "
+                                "one launch for all frames",
+                    "ms": dm, "steps_per_s": T / (dm * 1e-3), "frames_per_s": Bf * T / (dm * 1e-3),
+                    "us_per_step": dm * 1e3 / T}
+    log(f"fused CTC decode in one launch: {dm:.2f} ms, {fused_decode['us_per_step']:.2f} us/step, "
+        f"{fused_decode['frames_per_s']:.3g} frames/s")
+    del asr, asr_bt
 
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
@@ -242,6 +268,7 @@ def main():
                      "total_gbps": total_bytes / (mean_ms * 1e-3) / 1e9},
         "latency_b512_us": lat_us,
         "fused": fused,
+        "fused_decode": fused_decode,
         "cpu_baseline": cpu,
         "kernel_source_sha256": kernel_source_hash(),
     }

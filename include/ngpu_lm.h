@@ -153,6 +153,25 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
                               int32_t mode, float lambda, int32_t *d_states, int32_t *d_prev,
                               int32_t *d_tokens, void *hip_stream);
 
+/* A whole greedy decode (Section 2.3) in one launch: for each utterance b,
+ * frames t = 0 .. len_b - 1 run the rule of ngpu_lm_fused_greedy_step on the
+ * ASR row d_asr + b * stride_b + t * stride_t (strides in floats; the row holds
+ * classes 0..V-1 and, for CTC and transducer, blank = V), carrying the state
+ * and the previous label from frame to frame.
+ * d_lengths: [B] int32 frame counts (clamped to [0, T]) or NULL for T.
+ * In/out: d_states[B] (start states; final states on return), d_prev[B] (CTC:
+ *   the label before frame 0, blank = V for a new utterance; the last label on
+ *   return; may be NULL otherwise).  Passing the returned states and labels
+ *   back continues a decode exactly where it stopped.
+ * Out: d_labels[B, T] int32 (row b at d_labels + b * T): the label of each
+ *   frame, -1 past the utterance's length; d_label_states[B, T] (or NULL): the
+ *   state after each frame.  An out-of-range start state gives a row of -1 and
+ *   is counted for ngpu_lm_check_states.  Asynchronous on hip_stream. */
+int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t T, int64_t stride_b,
+                                int64_t stride_t, const int32_t *d_lengths, int32_t mode, float lambda,
+                                int32_t *d_states, int32_t *d_prev, int32_t *d_labels, int32_t *d_label_states,
+                                void *hip_stream);
+
 /* Synchronises hip_stream, then reports (and clears) how many out-of-range
  * input states the queries enqueued since the last check met.  Returns
  * NGPU_E_BAD_STATE when the count is non-zero. */

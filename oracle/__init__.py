@@ -60,7 +60,7 @@ def load(path: str = LIB_PATH):
                                        ctypes.c_float, vp, vp, vp]
     lib.oracle_greedy_step.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
-                                  ctypes.c_int, ctypes.c_float, vp, vp, vp, ctypes.c_int]
+                                  ctypes.c_int, ctypes.c_float, vp, vp, vp, vp, vp, ctypes.c_int]
     lib.oracle_decode.restype = ctypes.c_int
     lib.oracle_last_error.restype = ctypes.c_char_p
     _lib_cache[path] = lib
@@ -152,19 +152,24 @@ class Oracle:
             raise OracleError(rc, "greedy_step")
         return tok
 
-    def decode(self, asr, mode, lam, starts=None, nthreads: int = 1):
+    def decode(self, asr, mode, lam, starts=None, nthreads: int = 1, lengths=None, prev=None):
         """Greedy decode of ``asr`` [B, T, C] from ``starts`` [B] (default: the empty context).
 
+        ``lengths`` [B] limits the frames per utterance (later labels are -1);
+        ``prev`` [B] is the label before frame 0 (default blank = V).
         Returns per-frame labels and the state after each frame, both [B, T]."""
         asr = np.ascontiguousarray(asr, np.float32)
         B, T, C = asr.shape
         labels = np.empty((B, T), np.int32)
         st = np.empty((B, T), np.int32)
-        if starts is not None:
-            starts = np.ascontiguousarray(starts, np.int32)
-            assert len(starts) == B
+        arrs = []
+        for a in (starts, lengths, prev):
+            if a is not None:
+                a = np.ascontiguousarray(a, np.int32)
+                assert len(a) == B
+            arrs.append(a)
         rc = self._lib.oracle_decode(self._h, _ptr(asr), B, T, C, int(mode), float(lam),
-                                     _ptr(starts) if starts is not None else None,
+                                     *[_ptr(a) if a is not None else None for a in arrs],
                                      _ptr(labels), _ptr(st), int(nthreads))
         if rc != 0:
             raise OracleError(rc, "decode")

@@ -362,7 +362,7 @@ typedef struct {
     int64_t T, ld, b0, b1;
     int mode;
     float lambda;
-    const int32_t *starts;
+    const int32_t *starts, *lengths, *prev0;
     int32_t *labels, *states_out;
     int rc;
 } dec_job;
@@ -374,11 +374,14 @@ static void *dec_worker(void *p) {
     int32_t *nx = (int32_t *)malloc(sizeof(int32_t) * (size_t)m->V);
     if (!lm || !nx) { free(lm); free(nx); j->rc = OR_NOMEM; return NULL; }
     for (int64_t b = j->b0; b < j->b1; ++b) {
-        int32_t s = j->starts ? j->starts[b] : 0, prev = m->V;
+        int32_t s = j->starts ? j->starts[b] : 0, prev = j->prev0 ? j->prev0[b] : m->V;
         if (s < 0 || s >= m->S) { j->rc = OR_BAD_STATE; break; }
+        int64_t len = j->lengths ? j->lengths[b] : j->T;
+        if (len < 0) len = 0;
+        if (len > j->T) len = j->T;
         for (int64_t t = 0; t < j->T; ++t) {
             const float *row = j->asr + (b * j->T + t) * j->ld;
-            j->labels[b * j->T + t] = greedy_one(m, row, j->mode, j->lambda, &s, &prev, lm, nx);
+            j->labels[b * j->T + t] = t < len ? greedy_one(m, row, j->mode, j->lambda, &s, &prev, lm, nx) : -1;
             j->states_out[b * j->T + t] = s;
         }
     }
@@ -388,15 +391,17 @@ static void *dec_worker(void *p) {
 
 /* Whole greedy decode: asr [B, T, ld]; labels and states after each frame [B, T].
  * Hypothesis b starts at starts[b] (state 0 when starts is NULL) with previous
- * label = blank (V). */
+ * label prev0[b] (blank = V when prev0 is NULL) and runs lengths[b] frames (T
+ * when lengths is NULL); later frames get label -1 and keep the state. */
 int oracle_decode(const oracle_model *m, const float *asr, int64_t B, int64_t T, int64_t ld, int mode,
-                  float lambda, const int32_t *starts, int32_t *labels, int32_t *states_out, int nthreads) {
+                  float lambda, const int32_t *starts, const int32_t *lengths, const int32_t *prev0,
+                  int32_t *labels, int32_t *states_out, int nthreads) {
     if (mode < 0 || mode > 2) return OR_BAD_ARG;
     nthreads = clamp_threads(nthreads, B);
     dec_job jobs[256];
     for (int t = 0; t < nthreads; ++t) {
-        dec_job d = {m, asr, T, ld, B * t / nthreads, B * (t + 1) / nthreads, mode, lambda, starts,
-                     labels, states_out, 0};
+        dec_job d = {m, asr, T, ld, B * t / nthreads, B * (t + 1) / nthreads, mode, lambda, starts, lengths,
+                     prev0, labels, states_out, 0};
         jobs[t] = d;
     }
     run_jobs(dec_worker, jobs, sizeof(dec_job), nthreads);

@@ -30,7 +30,8 @@ ERROR_NAMES = {
 
 EXPORTED = [
     "ngpu_lm_build", "ngpu_lm_free", "ngpu_lm_info", "ngpu_lm_state_context", "ngpu_lm_device_bytes",
-    "ngpu_lm_upload", "ngpu_lm_advance", "ngpu_lm_fused_greedy_step", "ngpu_lm_check_states",
+    "ngpu_lm_upload", "ngpu_lm_advance", "ngpu_lm_fused_greedy_step", "ngpu_lm_fused_greedy_decode",
+    "ngpu_lm_check_states",
     "ngpu_lm_query_bytes", "ngpu_lm_host_image", "ngpu_lm_last_error",
 ]
 
@@ -77,6 +78,8 @@ def load_library(path: str = LIB_PATH):
     lib.ngpu_lm_upload.argtypes = [vp, vp, ctypes.c_size_t, vp]
     lib.ngpu_lm_advance.argtypes = [vp, vp, i64, vp, vp, vp]
     lib.ngpu_lm_fused_greedy_step.argtypes = [vp, vp, i64, i64, i32, ctypes.c_float, vp, vp, vp, vp]
+    lib.ngpu_lm_fused_greedy_decode.argtypes = [vp, vp, i64, i64, i64, i64, vp, i32, ctypes.c_float,
+                                                vp, vp, vp, vp, vp]
     lib.ngpu_lm_check_states.argtypes = [vp, vp, ctypes.POINTER(i64)]
     lib.ngpu_lm_query_bytes.argtypes = [vp, vp, i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ngpu_lm_host_image.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(ctypes.c_size_t)]
@@ -200,6 +203,36 @@ class NgpuLM:
             _dptr(prev, torch.int32, "prev") if prev is not None else None,
             _dptr(tokens, torch.int32, "tokens"), _stream_handle(stream)))
         return tokens
+
+    def fused_greedy_decode(self, asr, lam: float, states, prev=None, lengths=None,
+                            mode: int = NGPU_FUSION_PLAIN, labels=None, label_states=None, stream=None):
+        """Greedy decode of ``asr`` [B, T, C] (last dimension contiguous) in one launch.
+
+        ``states`` (and ``prev`` for CTC) are updated in place to the final
+        state (and label).  Returns labels [B, T] int32 (-1 past ``lengths``)."""
+        import torch
+        if asr.dim() != 3 or asr.stride(2) != 1 or asr.dtype != torch.float32 or not asr.is_cuda:
+            raise TypeError("asr must be a float32 [B, T, C] device tensor with unit class stride")
+        B, T, _ = asr.shape
+        if states.numel() != B or (prev is not None and prev.numel() != B):
+            raise ValueError("states/prev must hold B entries")
+        if labels is None:
+            labels = torch.empty((B, T), dtype=torch.int32, device=asr.device)
+        if labels.numel() != B * T:
+            raise ValueError("labels must hold B * T entries")
+        if label_states is not None and label_states.numel() != B * T:
+            raise ValueError("label_states must hold B * T entries")
+        if lengths is not None and lengths.numel() != B:
+            raise ValueError("lengths must hold B entries")
+        _check(self._lib.ngpu_lm_fused_greedy_decode(
+            self._h, ctypes.c_void_p(asr.data_ptr()), B, T, asr.stride(0), asr.stride(1),
+            _dptr(lengths, torch.int32, "lengths") if lengths is not None else None, int(mode), float(lam),
+            _dptr(states, torch.int32, "states"),
+            _dptr(prev, torch.int32, "prev") if prev is not None else None,
+            _dptr(labels, torch.int32, "labels"),
+            _dptr(label_states, torch.int32, "label_states") if label_states is not None else None,
+            _stream_handle(stream)))
+        return labels
 
     def check_states(self, stream=None) -> int:
         n = ctypes.c_int64()

@@ -146,8 +146,6 @@ int rows_per_block(int V, int want) {
     return h;
 }
 
-int advance_rows_per_block(int V) { return rows_per_block(V, 4); }
-
 hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, float *scores, int32_t *next,
                           hipStream_t stream) {
     const bool vec = (t.vocab_size % 4 == 0) && (reinterpret_cast<uintptr_t>(scores) % 16 == 0) &&

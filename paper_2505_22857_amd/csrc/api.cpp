@@ -14,6 +14,9 @@ hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, fl
                           hipStream_t stream);
 hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int64_t ld, int mode, float lambda,
                              int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream);
+hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
+                               const int32_t *lengths, int mode, float lambda, int32_t *states, int32_t *prev,
+                               int32_t *labels, int32_t *label_states, hipStream_t stream);
 }  // namespace ngpu
 
 namespace {
@@ -176,6 +179,33 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
     hipError_t e = ngpu::launch_fused_step(t, d_asr, B, asr_ld, mode, lambda, d_states, d_prev, d_tokens,
                                            static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return hip_fail(e, "fused step launch");
+    return ok();
+}
+
+int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t T, int64_t stride_b,
+                                int64_t stride_t, const int32_t *d_lengths, int32_t mode, float lambda,
+                                int32_t *d_states, int32_t *d_prev, int32_t *d_labels, int32_t *d_label_states,
+                                void *hip_stream) {
+    if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_TRANSDUCER)
+        return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
+    if (B < 0 || B > INT32_MAX || T < 0) return fail(NGPU_E_INVALID_ARG, "bad sizes B=%lld T=%lld", (long long)B,
+                                                     (long long)T);
+    if (stride_b < 0 || stride_t < 0) return fail(NGPU_E_INVALID_ARG, "negative strides");
+    const int64_t need = mode == NGPU_FUSION_PLAIN ? lm->V : int64_t(lm->V) + 1;
+    if (T > 1 && stride_t < need) return fail(NGPU_E_INVALID_ARG, "stride_t %lld < %lld", (long long)stride_t,
+                                              (long long)need);
+    if (B > 1 && stride_b < need) return fail(NGPU_E_INVALID_ARG, "stride_b %lld < %lld", (long long)stride_b,
+                                              (long long)need);
+    if (!std::isfinite(lambda)) return fail(NGPU_E_INVALID_ARG, "lambda must be finite");
+    if (B == 0 || T == 0) return ok();
+    if (!d_asr || !d_states || !d_labels || (mode == NGPU_FUSION_CTC && !d_prev))
+        return fail(NGPU_E_INVALID_ARG, "null device pointer");
+    const ngpu::DevTrie t = dev_view(lm);
+    hipError_t e = ngpu::launch_fused_decode(t, d_asr, B, T, stride_b, stride_t, d_lengths, mode, lambda, d_states,
+                                             d_prev, d_labels, d_label_states, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "fused decode launch");
     return ok();
 }
 

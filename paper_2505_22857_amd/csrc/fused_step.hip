@@ -1,4 +1,5 @@
-// One greedy shallow-fusion step (Section 2.3) over a batch of hypotheses.
+// Greedy shallow fusion (Section 2.3): one step over a batch of hypotheses, and
+// a whole decode over all frames of a batch of utterances in one launch.
 //
 // One wavefront per hypothesis.  CTC and transducer modes first take the plain
 // ASR argmax over the V + 1 classes; when that keeps blank (or, for CTC, the
@@ -9,6 +10,10 @@
 // token and reduces to the argmax with lowest-index ties through 64-bit keys
 // (value, ~index) and cross-lane shuffles.  The winner's next state comes from
 // the same merge.  No MFMA: one fma and one compare per token.
+//
+// The decode kernel keeps each utterance's state and previous label in
+// registers across frames: frame t + 1 depends on frame t only through them,
+// so a single launch replaces T launches and their host round trips.
 #include <hip/hip_runtime.h>
 
 #include "walk.h"
@@ -16,6 +21,43 @@
 namespace ngpu {
 
 enum { kPlain = 0, kCtc = 1, kTransducer = 2 };
+
+// One fused greedy step of the wavefront's hypothesis on ASR row `row`.
+// s: valid state (uniform); pv: previous label (CTC).  Returns the label and
+// updates s.  All lanes return the same values.
+template <int MODE>
+__device__ __forceinline__ int greedy_step(const DevTrie &t, const float *__restrict__ row, float lambda, int &s,
+                                           int pv, float *ls, int *ln, int lane) {
+    const int V = t.vocab_size;
+    if (MODE != kPlain) {
+        unsigned long long best = 0;
+        for (int v = lane; v <= V; v += kWave) {
+            const unsigned long long k = argmax_key(row[v], v);
+            best = k > best ? k : best;
+        }
+        const int a = argmax_index(wave_max_u64(best));
+        if (a == V || (MODE == kCtc && a == pv)) return a;   // blank or repeat: no LM, no move
+    }
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
+    const float *dw = t.dense_w + size_t(h.dense_row) * V;
+    const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
+    unsigned long long best = 0;
+    for (int v = lane; v < V; v += kWave) {
+        float lm;
+        int n;
+        merge_slot(h, ls[v], ln[v], dw[v], dt[v], lm, n);
+        const float f = __builtin_fmaf(lambda, lm, row[v]);
+        if (MODE == kCtc && v == pv) continue;
+        const unsigned long long k = argmax_key(f, v);
+        best = k > best ? k : best;
+    }
+    const int w = argmax_index(wave_max_u64(best));
+    float lm;
+    int n;
+    merge_slot(h, ls[w], ln[w], dw[w], dt[w], lm, n);   // uniform w: every lane reads the same slot
+    s = n;
+    return w;
+}
 
 template <int HPB, int MODE>
 __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, const float *__restrict__ asr,
@@ -31,9 +73,8 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
     const int V = t.vocab_size;
     float *ls = lds + size_t(wave) * 2 * V;
     int *ln = reinterpret_cast<int *>(ls + V);
-    const float *row = asr + b * ld;
 
-    const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    int s = __builtin_amdgcn_readfirstlane(states[b]);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) {
             atomicAdd(&t.status[0], 1);
@@ -41,46 +82,66 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
         }
         return;
     }
-    int pv = -1;
-    if (MODE == kCtc) pv = __builtin_amdgcn_readfirstlane(prev[b]);
-
-    if (MODE != kPlain) {
-        unsigned long long best = 0;
-        for (int v = lane; v <= V; v += kWave) {
-            const unsigned long long k = argmax_key(row[v], v);
-            best = k > best ? k : best;
-        }
-        const int a = argmax_index(wave_max_u64(best));
-        if (a == V || (MODE == kCtc && a == pv)) {
-            if (lane == 0) {
-                tokens[b] = a;
-                if (MODE == kCtc) prev[b] = a;
-            }
-            return;
-        }
-    }
-
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
-    const float *dw = t.dense_w + size_t(h.dense_row) * V;
-    const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
-    unsigned long long best = 0;
-    for (int v = lane; v < V; v += kWave) {
-        float lm;
-        int n;
-        merge_slot(h, ls[v], ln[v], dw[v], dt[v], lm, n);
-        const float f = __builtin_fmaf(lambda, lm, row[v]);
-        if (MODE == kCtc && v == pv) continue;
-        const unsigned long long k = argmax_key(f, v);
-        best = k > best ? k : best;
-    }
-    const int w = argmax_index(wave_max_u64(best));
+    const int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
+    const int label = greedy_step<MODE>(t, asr + b * ld, lambda, s, pv, ls, ln, lane);
     if (lane == 0) {
-        float lm;
-        int n;
-        merge_slot(h, ls[w], ln[w], dw[w], dt[w], lm, n);
-        states[b] = n;
-        tokens[b] = w;
-        if (MODE == kCtc) prev[b] = w;
+        tokens[b] = label;
+        states[b] = s;
+        if (MODE == kCtc) prev[b] = label;
+    }
+}
+
+// Whole greedy decode: utterance b runs frames 0 .. len_b - 1 of
+// asr[b * stride_b + t * stride_t + class].
+template <int MODE>
+__global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
+                                                              int64_t T, int64_t stride_b, int64_t stride_t,
+                                                              const int32_t *__restrict__ lengths, float lambda,
+                                                              int32_t *__restrict__ states,
+                                                              int32_t *__restrict__ prev,
+                                                              int32_t *__restrict__ labels,
+                                                              int32_t *__restrict__ label_states) {
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    if (b >= B) return;
+    const int V = t.vocab_size;
+    float *ls = lds;
+    int *ln = reinterpret_cast<int *>(ls + V);
+    int32_t *lab = labels + b * T;
+    int32_t *lst = label_states ? label_states + b * T : nullptr;
+
+    int64_t len = T;
+    if (lengths) {
+        len = __builtin_amdgcn_readfirstlane(lengths[b]);
+        len = len < 0 ? 0 : (len > T ? T : len);
+    }
+    int s = __builtin_amdgcn_readfirstlane(states[b]);
+    if (s < 0 || s >= t.num_states) {
+        if (lane == 0) atomicAdd(&t.status[0], 1);
+        for (int64_t f = lane; f < T; f += kWave) {
+            lab[f] = -1;
+            if (lst) lst[f] = -1;
+        }
+        return;
+    }
+    int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
+    const float *row = asr + b * stride_b;
+    for (int64_t f = 0; f < len; ++f, row += stride_t) {
+        const int label = greedy_step<MODE>(t, row, lambda, s, pv, ls, ln, lane);
+        if (MODE == kCtc) pv = label;
+        if (lane == 0) {
+            lab[f] = label;
+            if (lst) lst[f] = s;
+        }
+    }
+    for (int64_t f = len + lane; f < T; f += kWave) {   // frames past the utterance's end
+        lab[f] = -1;
+        if (lst) lst[f] = s;
+    }
+    if (lane == 0) {
+        states[b] = s;
+        if (MODE == kCtc) prev[b] = pv;
     }
 }
 
@@ -94,24 +155,40 @@ static hipError_t launch_one(const DevTrie &t, const float *asr, int64_t B, int6
     return hipGetLastError();
 }
 
-int advance_rows_per_block(int V);
-
-template <int MODE>
-static hipError_t launch_mode(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
-                              int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
-    switch (advance_rows_per_block(t.vocab_size)) {
-        case 4: return launch_one<4, MODE>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        case 2: return launch_one<2, MODE>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        default: return launch_one<1, MODE>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-    }
-}
-
+// One hypothesis per workgroup: a step batch is a few hundred hypotheses, so
+// spreading them over all CUs beats packing them.
 hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int64_t ld, int mode, float lambda,
                              int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
     switch (mode) {
-        case kPlain: return launch_mode<kPlain>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        case kCtc: return launch_mode<kCtc>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        default: return launch_mode<kTransducer>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        case kPlain: return launch_one<1, kPlain>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        case kCtc: return launch_one<1, kCtc>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        default: return launch_one<1, kTransducer>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+    }
+}
+
+template <int MODE>
+static hipError_t launch_decode_mode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb,
+                                     int64_t st, const int32_t *lengths, float lambda, int32_t *states,
+                                     int32_t *prev, int32_t *labels, int32_t *label_states, hipStream_t stream) {
+    const size_t lds = 2 * size_t(t.vocab_size) * sizeof(float);
+    hipLaunchKernelGGL((fused_decode_kernel<MODE>), dim3(unsigned(B)), dim3(kWave), lds, stream, t, asr, B, T, sb,
+                       st, lengths, lambda, states, prev, labels, label_states);
+    return hipGetLastError();
+}
+
+hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
+                               const int32_t *lengths, int mode, float lambda, int32_t *states, int32_t *prev,
+                               int32_t *labels, int32_t *label_states, hipStream_t stream) {
+    switch (mode) {
+        case kPlain:
+            return launch_decode_mode<kPlain>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                              label_states, stream);
+        case kCtc:
+            return launch_decode_mode<kCtc>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                            label_states, stream);
+        default:
+            return launch_decode_mode<kTransducer>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                                   label_states, stream);
     }
 }
 

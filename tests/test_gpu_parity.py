@@ -233,14 +233,112 @@ def test_fused_plain_cfg2_with_advance_every_step(dev):
     check_advance("cfg2 states along the decode", m, lm, o, visited, dev)
 
 
+_CFG5 = {}
+
+
+def cfg5_data():
+    """Config 5: the ASR tensor and the oracle's decode of it, computed once."""
+    if not _CFG5:
+        m, lm, o = cfg_pair(4)
+        spec = CONFIGS[5]
+        V = m.vocab_size
+        asr = asr_logprobs((spec.batch, spec.steps, V + 1), seed=seed_for(5), blank_boost=spec.blank_boost)
+        _CFG5["asr"] = asr
+        _CFG5["oracle"] = o.decode(asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), nthreads=NTHREADS)
+    return _CFG5["asr"], _CFG5["oracle"]
+
+
 def test_fused_ctc_cfg5(dev):
     m, lm, o = cfg_pair(4)
     spec = CONFIGS[5]
     V = m.vocab_size
-    asr = asr_logprobs((spec.batch, spec.steps, V + 1), seed=seed_for(5), blank_boost=spec.blank_boost)
-    gl, _ = check_decode("ctc cfg5", lm, o, asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), dev)
-    blank = (gl == V).mean()
-    print(f"  cfg5: blank labels {blank:.3f}", flush=True)
+    asr, (ol, os_) = cfg5_data()
+    case(f"fused ctc cfg5 per-frame steps B={spec.batch} T={spec.steps}")
+    gl, gs = gpu_decode(lm, asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), dev)
+    assert lm.check_states() == 0
+    assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+    print(f"  cfg5 per-frame: {gl.size} decisions identical, blank labels {(gl == V).mean():.3f}", flush=True)
+
+
+# ------------------------------------------------------------------ whole decode in one launch
+
+def gpu_decode_launch(lm, asr_np, mode, lam, starts, dev, lengths=None, prev0=None):
+    B, T, C = asr_np.shape
+    asr = torch.from_numpy(asr_np).to(dev)
+    st = torch.from_numpy(np.ascontiguousarray(starts, np.int32)).to(dev)
+    prev = None
+    if mode == MODE_CTC:
+        p0 = np.full(B, lm.vocab_size, np.int32) if prev0 is None else prev0
+        prev = torch.from_numpy(np.ascontiguousarray(p0, np.int32)).to(dev)
+    ln = torch.from_numpy(np.ascontiguousarray(lengths, np.int32)).to(dev) if lengths is not None else None
+    lst = torch.full((B, T), -9, dtype=torch.int32, device=dev)
+    lab = lm.fused_greedy_decode(asr, lam, st, prev, lengths=ln, mode=mode, label_states=lst)
+    torch.cuda.synchronize()
+    return (lab.cpu().numpy(), lst.cpu().numpy(), st.cpu().numpy(),
+            prev.cpu().numpy() if prev is not None else None)
+
+
+def test_decode_launch_ctc_cfg5(dev):
+    m, lm, o = cfg_pair(4)
+    spec = CONFIGS[5]
+    asr, (ol, os_) = cfg5_data()
+    case(f"decode launch ctc cfg5 B={spec.batch} T={spec.steps}")
+    gl, gs, fin, fprev = gpu_decode_launch(lm, asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), dev)
+    assert lm.check_states() == 0
+    bad = np.argwhere(gl != ol)
+    assert len(bad) == 0, f"labels differ first at {bad[0]}"
+    assert np.array_equal(gs, os_)
+    assert np.array_equal(fin, os_[:, -1]) and np.array_equal(fprev, ol[:, -1])
+    print(f"  cfg5 one launch: {gl.size} decisions identical", flush=True)
+
+
+@pytest.mark.parametrize("mode", [MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER])
+def test_decode_launch_modes_ragged_lengths(dev, mode):
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    B, T = 37, 90
+    starts = uniform_states(m, B, seed=31)
+    C = V if mode == MODE_PLAIN else V + 1
+    asr = asr_logprobs((B, T, C), seed=32, blank_boost=2.0 if mode != MODE_PLAIN else 0.0)
+    lengths = np.random.default_rng(33).integers(0, T + 1, B).astype(np.int32)
+    lengths[:3] = [0, T, 1]
+    case(f"decode launch mode={mode} B={B} T={T} ragged")
+    gl, gs, fin, fprev = gpu_decode_launch(lm, asr, mode, 0.6, starts, dev, lengths=lengths)
+    assert lm.check_states() == 0
+    ol, os_ = o.decode(asr, mode, 0.6, starts, nthreads=NTHREADS, lengths=lengths)
+    assert np.array_equal(gl, ol)
+    assert np.array_equal(gs, os_)
+    assert np.array_equal(fin, os_[:, -1])
+
+
+def test_decode_launch_resumes_exactly(dev):
+    """Two launches over frames [0, 40) and [40, 90), passing states and labels
+    back, equal one decode over all 90 frames."""
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    B, T, cut = 24, 90, 40
+    starts = uniform_states(m, B, seed=41)
+    asr = asr_logprobs((B, T, V + 1), seed=42, blank_boost=2.0)
+    case("decode launch resume")
+    gl, gs, fin, fprev = gpu_decode_launch(lm, asr, MODE_CTC, 0.5, starts, dev)
+    a1, s1, f1, p1 = gpu_decode_launch(lm, np.ascontiguousarray(asr[:, :cut]), MODE_CTC, 0.5, starts, dev)
+    a2, s2, f2, p2 = gpu_decode_launch(lm, np.ascontiguousarray(asr[:, cut:]), MODE_CTC, 0.5, f1, dev, prev0=p1)
+    assert np.array_equal(np.concatenate([a1, a2], 1), gl)
+    assert np.array_equal(np.concatenate([s1, s2], 1), gs)
+    assert np.array_equal(f2, fin) and np.array_equal(p2, fprev)
+
+
+def test_decode_launch_bad_start_state(dev):
+    m, lm, o = cfg_pair(1)
+    V = m.vocab_size
+    asr = asr_logprobs((3, 7, V), seed=43)
+    starts = np.array([2, m.num_states, 5], np.int32)
+    case("decode launch with an out-of-range start state")
+    gl, gs, fin, _ = gpu_decode_launch(lm, asr, MODE_PLAIN, 0.5, starts, dev)
+    assert lm.check_states() == 1
+    assert (gl[1] == -1).all() and (gs[1] == -1).all()
+    ol, os_ = o.decode(asr[[0, 2]], MODE_PLAIN, 0.5, starts[[0, 2]])
+    assert np.array_equal(gl[[0, 2]], ol) and np.array_equal(gs[[0, 2]], os_)
 
 
 def test_fused_transducer_and_ctc_small(dev):

@@ -1,11 +1,11 @@
 // Batched full-vocabulary backoff query (Algorithm 1, batched over hypotheses).
 //
 // One wavefront per hypothesis, HPB wavefronts per workgroup, each with its
-// own V-wide score/state row in LDS (8 bytes per token).  After the sparse
-// levels are scattered, the row is merged with the order-1 ancestor's dense
-// row and written to HBM with 16-byte stores (when V is a multiple of 4):
-// lane l covers tokens 4l..4l+3 of each 256-token stripe, so one store
-// instruction of the wavefront writes 1 KiB contiguously.
+// own V-wide score/state row in LDS (8 bytes per token).  After the walk
+// (dense row copied in, sparse levels applied on top), the row is written to
+// HBM with 16-byte non-temporal stores (when V is a multiple of 4): lane l
+// covers tokens 4l..4l+3 of each 256-token stripe, so one store instruction
+// of the wavefront writes 1 KiB contiguously.
 //
 // XCD-aware distribution (G = 8): workgroups are dispatched round-robin over
 // the eight XCDs, so workgroup i serves dense-row group i % 8.  Each wavefront
@@ -37,13 +37,11 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
     const int64_t base = (int64_t(blockIdx.x / G) * HPB + wave) * G;
     if (base >= B) return;  // whole wavefronts leave; no workgroup barrier is used
     const int V = t.vocab_size;
-    float *ls = lds + size_t(wave) * 2 * V;
-    int *ln = reinterpret_cast<int *>(ls + V);
+    float *ls = lds + size_t(wave) * 2 * lds_row(V);
+    int *ln = reinterpret_cast<int *>(ls + lds_row(V));
 
     // scan: lane i < G looks at hypothesis base + i
     int s_l = -1;
-    int4 head_l = make_int4(0, 0, 0, 0);
-    uint64_t rp_l = 0;
     bool mine = false;
     const int64_t bl = base + lane;
     if (lane < G && bl < B) {
@@ -51,11 +49,12 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
         if (s_l < 0 || s_l >= t.num_states) {
             s_l = -1;
             mine = (bl % G) == grp;   // an invalid state's row is written by one owner
+        } else if (G == 1) {
+            mine = true;
         } else {
-            const unsigned char *rp = chain_record(t, s_l);
-            rp_l = reinterpret_cast<uint64_t>(rp);
-            head_l = *reinterpret_cast<const int4 *>(rp);
-            mine = G == 1 || (head_l.w >> 16) == grp;
+            int nl;
+            const ChainHead hd = *reinterpret_cast<const ChainHead *>(chain_record(t, s_l, nl));
+            mine = chain_group(hd) == grp;
         }
     }
     uint64_t todo = __ballot(mine);
@@ -74,39 +73,29 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
             }
             continue;
         }
-        ChainHead h;
-        h.dense_row = __builtin_amdgcn_readlane(head_l.x, i);
-        h.acc1 = __int_as_float(__builtin_amdgcn_readlane(head_l.y, i));
-        h.acc0 = __int_as_float(__builtin_amdgcn_readlane(head_l.z, i));
-        h.nlev_group = __builtin_amdgcn_readlane(head_l.w, i);
-        const uint64_t rpu = (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(rp_l >> 32), i))) << 32) |
-                             uint32_t(__builtin_amdgcn_readlane(int(rp_l & 0xffffffffu), i));
-        scatter_levels(t, reinterpret_cast<const unsigned char *>(rpu), chain_levels(h), ls, ln, lane);
-        const float *dw = t.dense_w + size_t(h.dense_row) * V;
-        const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
-
+        const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
         if (VEC) {
             for (int v = lane * 4; v < V; v += 4 * kWave) {
                 const int4 n4 = *reinterpret_cast<const int4 *>(ln + v);
                 const float4 x4 = *reinterpret_cast<const float4 *>(ls + v);
-                const float4 w4 = *reinterpret_cast<const float4 *>(dw + v);
-                const int4 t4 = *reinterpret_cast<const int4 *>(dt + v);
-                float4 xo;
-                int4 no;
-                merge_slot(h, x4.x, n4.x, w4.x, t4.x, xo.x, no.x);
-                merge_slot(h, x4.y, n4.y, w4.y, t4.y, xo.y, no.y);
-                merge_slot(h, x4.z, n4.z, w4.z, t4.z, xo.z, no.z);
-                merge_slot(h, x4.w, n4.w, w4.w, t4.w, xo.w, no.w);
+                nf4 xo;
+                ni4 no;
+                float x;
+                int n;
+                slot_value(h, x4.x, n4.x, x, n); xo.x = x; no.x = n;
+                slot_value(h, x4.y, n4.y, x, n); xo.y = x; no.y = n;
+                slot_value(h, x4.z, n4.z, x, n); xo.z = x; no.z = n;
+                slot_value(h, x4.w, n4.w, x, n); xo.w = x; no.w = n;
                 // streaming stores: the rows are not read again here, so they
                 // should not displace the dense rows and arcs from the L2
-                __builtin_nontemporal_store(nf4{xo.x, xo.y, xo.z, xo.w}, reinterpret_cast<nf4 *>(orow + v));
-                __builtin_nontemporal_store(ni4{no.x, no.y, no.z, no.w}, reinterpret_cast<ni4 *>(nrow + v));
+                __builtin_nontemporal_store(xo, reinterpret_cast<nf4 *>(orow + v));
+                __builtin_nontemporal_store(no, reinterpret_cast<ni4 *>(nrow + v));
             }
         } else {
             for (int v = lane; v < V; v += kWave) {
                 float x;
                 int n;
-                merge_slot(h, ls[v], ln[v], dw[v], dt[v], x, n);
+                slot_value(h, ls[v], ln[v], x, n);
                 __builtin_nontemporal_store(x, orow + v);
                 __builtin_nontemporal_store(n, nrow + v);
             }
@@ -119,7 +108,7 @@ static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B,
                              int32_t *next, hipStream_t stream, bool vec) {
     const int64_t chunks = (B + int64_t(HPB) * G - 1) / (int64_t(HPB) * G);
     const dim3 grid(unsigned(chunks * G)), block(HPB * kWave);
-    const size_t lds = size_t(HPB) * 2 * size_t(t.vocab_size) * sizeof(float);
+    const size_t lds = size_t(HPB) * 2 * size_t(lds_row(t.vocab_size)) * sizeof(float);
     if (vec)
         hipLaunchKernelGGL((advance_kernel<HPB, true, G>), grid, block, lds, stream, t, states, B, scores, next);
     else
@@ -140,7 +129,7 @@ constexpr int kHpbPlain = 2;
 
 // Wavefronts per workgroup: at most `want`, as many rows as fit in 32 KiB of LDS.
 int rows_per_block(int V, int want) {
-    const size_t row = size_t(V) * 8;
+    const size_t row = size_t(lds_row(V)) * 8;
     int h = want;
     while (h > 1 && size_t(h) * row > 32768) h /= 2;
     return h;

@@ -27,7 +27,8 @@ enum { kPlain = 0, kCtc = 1, kTransducer = 2 };
 // updates s.  All lanes return the same values.
 template <int MODE>
 __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *__restrict__ row, float lambda, int &s,
-                                           int pv, float *ls, int *ln, int lane) {
+                                           int pv, float *ls, int *ln, int lane, const float *pf_src = nullptr,
+                                           float *pf_dst = nullptr, int pf_n = 0) {
     const int V = t.vocab_size;
     if (MODE != kPlain) {
         unsigned long long best = 0;
@@ -36,16 +37,17 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *__rest
             best = k > best ? k : best;
         }
         const int a = argmax_index(wave_max_u64(best));
-        if (a == V || (MODE == kCtc && a == pv)) return a;   // blank or repeat: no LM, no move
+        if (a == V || (MODE == kCtc && a == pv)) {   // blank or repeat: no LM, no move
+            if (pf_src) copy_to_lds_dword(pf_src, pf_dst, pf_n, lane);
+            return a;
+        }
     }
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
-    const float *dw = t.dense_w + size_t(h.dense_row) * V;
-    const int32_t *dt = t.dense_to + size_t(h.dense_row) * V;
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane, pf_src, pf_dst, pf_n);
     unsigned long long best = 0;
     for (int v = lane; v < V; v += kWave) {
         float lm;
         int n;
-        merge_slot(h, ls[v], ln[v], dw[v], dt[v], lm, n);
+        slot_value(h, ls[v], ln[v], lm, n);
         const float f = __builtin_fmaf(lambda, lm, row[v]);
         if (MODE == kCtc && v == pv) continue;
         const unsigned long long k = argmax_key(f, v);
@@ -54,7 +56,7 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *__rest
     const int w = argmax_index(wave_max_u64(best));
     float lm;
     int n;
-    merge_slot(h, ls[w], ln[w], dw[w], dt[w], lm, n);   // uniform w: every lane reads the same slot
+    slot_value(h, ls[w], ln[w], lm, n);   // uniform w: every lane reads the same slot
     s = n;
     return w;
 }
@@ -71,8 +73,8 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
     const int64_t b = int64_t(blockIdx.x) * HPB + wave;
     if (b >= B) return;
     const int V = t.vocab_size;
-    float *ls = lds + size_t(wave) * 2 * V;
-    int *ln = reinterpret_cast<int *>(ls + V);
+    float *ls = lds + size_t(wave) * 2 * lds_row(V);
+    int *ln = reinterpret_cast<int *>(ls + lds_row(V));
 
     int s = __builtin_amdgcn_readfirstlane(states[b]);
     if (s < 0 || s >= t.num_states) {
@@ -106,8 +108,11 @@ __global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const fl
     const int64_t b = blockIdx.x;
     if (b >= B) return;
     const int V = t.vocab_size;
+    const int C = V + 1;                       // ASR row words used (V for plain fusion suffices)
+    const int rowp = (C + kWave - 1) & ~(kWave - 1);
     float *ls = lds;
-    int *ln = reinterpret_cast<int *>(ls + V);
+    int *ln = reinterpret_cast<int *>(ls + lds_row(V));
+    float *abuf = reinterpret_cast<float *>(ln + lds_row(V));   // two ASR rows, double-buffered
     int32_t *lab = labels + b * T;
     int32_t *lst = label_states ? label_states + b * T : nullptr;
 
@@ -127,8 +132,14 @@ __global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const fl
     }
     int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
     const float *row = asr + b * stride_b;
+    const int cn = MODE == kPlain ? V : C;
+    if (len > 0) copy_to_lds_dword(row, abuf, cn, lane);
     for (int64_t f = 0; f < len; ++f, row += stride_t) {
-        const int label = greedy_step<MODE>(t, row, lambda, s, pv, ls, ln, lane);
+        // frame f reads its ASR row from LDS; the walk also starts the copy of row f + 1
+        float *cur = abuf + (f & 1) * rowp;
+        float *nxt = abuf + ((f + 1) & 1) * rowp;
+        const float *pf = f + 1 < len ? row + stride_t : nullptr;
+        const int label = greedy_step<MODE>(t, cur, lambda, s, pv, ls, ln, lane, pf, nxt, cn);
         if (MODE == kCtc) pv = label;
         if (lane == 0) {
             lab[f] = label;
@@ -149,7 +160,7 @@ template <int HPB, int MODE>
 static hipError_t launch_one(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
                              int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
     const int64_t blocks = (B + HPB - 1) / HPB;
-    const size_t lds = size_t(HPB) * 2 * size_t(t.vocab_size) * sizeof(float);
+    const size_t lds = size_t(HPB) * 2 * size_t(lds_row(t.vocab_size)) * sizeof(float);
     hipLaunchKernelGGL((fused_step_kernel<HPB, MODE>), dim3(unsigned(blocks)), dim3(HPB * kWave), lds, stream,
                        t, asr, B, ld, lambda, states, prev, tokens);
     return hipGetLastError();
@@ -170,7 +181,8 @@ template <int MODE>
 static hipError_t launch_decode_mode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb,
                                      int64_t st, const int32_t *lengths, float lambda, int32_t *states,
                                      int32_t *prev, int32_t *labels, int32_t *label_states, hipStream_t stream) {
-    const size_t lds = 2 * size_t(t.vocab_size) * sizeof(float);
+    const size_t rowp = size_t((t.vocab_size + 1 + kWave - 1) & ~(kWave - 1));
+    const size_t lds = (2 * size_t(lds_row(t.vocab_size)) + 2 * rowp) * sizeof(float);
     hipLaunchKernelGGL((fused_decode_kernel<MODE>), dim3(unsigned(B)), dim3(kWave), lds, stream, t, asr, B, T, sb,
                        st, lengths, lambda, states, prev, labels, label_states);
     return hipGetLastError();

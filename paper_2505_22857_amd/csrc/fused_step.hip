@@ -135,7 +135,9 @@ __global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const fl
     const int cn = MODE == kPlain ? V : C;
     if (len > 0) copy_to_lds_dword(row, abuf, cn, lane);
     for (int64_t f = 0; f < len; ++f, row += stride_t) {
-        // frame f reads its ASR row from LDS; the walk also starts the copy of row f + 1
+        // frame f reads its ASR row from LDS, copied during frame f - 1 (or
+        // before the loop); the walk also starts the copy of row f + 1
+        wait_lds_copies();
         float *cur = abuf + (f & 1) * rowp;
         float *nxt = abuf + ((f + 1) & 1) * rowp;
         const float *pf = f + 1 < len ? row + stride_t : nullptr;

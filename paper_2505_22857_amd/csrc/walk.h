@@ -19,8 +19,9 @@
 //      flagged as backed off to the empty context, else acc1.
 // Races: tokens within a level are distinct, so lanes never write the same
 // slot in one level; LDS operations of one wavefront complete in program
-// order, and the compiler waits for the global -> LDS copies (vmcnt) before the
-// first LDS access that may touch their destination.
+// order.  A global -> LDS copy lands asynchronously: the sparse writes wait
+// for their own arc loads, issued after the copy (vector memory loads complete
+// in order), and every reader of copied data first calls wait_lds_copies().
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -34,9 +35,12 @@ constexpr int kArcUnroll = 4;                  // arc stripes of 64 lanes loaded
 constexpr int32_t kFinal = 0x40000000;         // ln bit: slot written by a sparse level
 constexpr int32_t kStateMask = 0x3fffffff;
 
-// s_waitcnt vmcnt(0) with the other counters left alone (gfx9 encoding:
-// vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]).
-constexpr int kWaitVmcnt0 = (7 << 4) | (15 << 8);
+// Waits until every global -> LDS copy (and every other vector memory access)
+// of this wavefront has completed.  The compiler does not reliably order LDS
+// reads after those copies by itself, so every reader of copied data waits
+// here first; the memory clobber keeps the compiler from moving any memory
+// access across the wait.
+__device__ __forceinline__ void wait_lds_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 typedef __attribute__((address_space(1))) const void global_cptr;
 typedef __attribute__((address_space(3))) void lds_ptr;
@@ -168,10 +172,10 @@ __device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, floa
             store_stripe(st, acc, ls, ln);
         }
     }
-    // Every copy into LDS has landed from here on.  Waiting once here keeps the
-    // readers' loops free of waits: on gfx950 stores count in vmcnt too, so a
-    // wait inside a loop that also stores would drain those stores each turn.
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    // Every copy into LDS has landed from here on.  Waiting once here also keeps
+    // the readers' loops free of waits: on gfx950 stores count in vmcnt too, so
+    // a wait inside a loop that also stores would drain those stores each turn.
+    wait_lds_copies();
     return h;
 }
 

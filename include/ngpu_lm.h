@@ -153,6 +153,22 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
                               int32_t mode, float lambda, int32_t *d_states, int32_t *d_prev,
                               int32_t *d_tokens, void *hip_stream);
 
+#define NGPU_LM_MAX_TOPK 256
+
+/* The k best tokens of the fused score fmaf(lambda, lm[v], asr[v]) over
+ * v < V for each hypothesis -- the expansion step of a beam search with the
+ * LM fused over the full vocabulary (Section 2.3: full-vocabulary scoring
+ * before selection; the paper applies it to AED beam search).  Row b of the
+ * outputs ([B, k] each, row-major) lists the k best in descending order of
+ * the fused score, ties to the lower token index: d_tokens (int32), d_scores
+ * (fp32 fused scores), d_next (int32 state after that token).  States are
+ * read only.  1 <= k <= min(V, NGPU_LM_MAX_TOPK); cost grows as k * V per
+ * hypothesis.  An out-of-range state gives a row of -1 tokens, NaN scores and
+ * -1 states and is counted for ngpu_lm_check_states.  Asynchronous. */
+int ngpu_lm_fused_topk(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t asr_ld, float lambda, int32_t k,
+                       const int32_t *d_states, int32_t *d_tokens, float *d_scores, int32_t *d_next,
+                       void *hip_stream);
+
 /* A whole greedy decode (Section 2.3) in one launch: for each utterance b,
  * frames t = 0 .. len_b - 1 run the rule of ngpu_lm_fused_greedy_step on the
  * ASR row d_asr + b * stride_b + t * stride_t (strides in floats; the row holds

@@ -62,6 +62,9 @@ def load(path: str = LIB_PATH):
     lib.oracle_decode.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                   ctypes.c_int, ctypes.c_float, vp, vp, vp, vp, vp, ctypes.c_int]
     lib.oracle_decode.restype = ctypes.c_int
+    lib.oracle_fused_topk.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_float, ctypes.c_int,
+                                      vp, vp, vp, vp]
+    lib.oracle_fused_topk.restype = ctypes.c_int
     lib.oracle_last_error.restype = ctypes.c_char_p
     _lib_cache[path] = lib
     return lib
@@ -151,6 +154,20 @@ class Oracle:
         if rc != 0:
             raise OracleError(rc, "greedy_step")
         return tok
+
+    def fused_topk(self, asr, lam, k, states):
+        """k best fused tokens per hypothesis: (tokens, scores, next states), each [B, k]."""
+        asr = np.ascontiguousarray(asr, np.float32)
+        B, ld = asr.shape
+        states = np.ascontiguousarray(states, np.int32)
+        tok = np.empty((B, k), np.int32)
+        sc = np.empty((B, k), np.float32)
+        nx = np.empty((B, k), np.int32)
+        rc = self._lib.oracle_fused_topk(self._h, _ptr(asr), B, ld, float(lam), int(k), _ptr(states),
+                                         _ptr(tok), _ptr(sc), _ptr(nx))
+        if rc != 0:
+            raise OracleError(rc, "fused_topk")
+        return tok, sc, nx
 
     def decode(self, asr, mode, lam, starts=None, nthreads: int = 1, lengths=None, prev=None):
         """Greedy decode of ``asr`` [B, T, C] from ``starts`` [B] (default: the empty context).

@@ -356,6 +356,38 @@ int oracle_greedy_step(const oracle_model *m, const float *asr, int64_t B, int64
     return rc;
 }
 
+/* The k best fused scores fmaf(lambda, lm(v), asr(v)) over v < V of each
+ * hypothesis, in descending order, ties to the lower index (a selection sort
+ * over the definition's row); states are not changed. */
+int oracle_fused_topk(const oracle_model *m, const float *asr, int64_t B, int64_t ld, float lambda, int k,
+                      const int32_t *states, int32_t *tokens, float *scores, int32_t *next) {
+    if (k < 1 || k > m->V) return OR_BAD_ARG;
+    int32_t V = m->V;
+    float *lm = (float *)malloc(sizeof(float) * (size_t)V);
+    float *f = (float *)malloc(sizeof(float) * (size_t)V);
+    int32_t *nx = (int32_t *)malloc(sizeof(int32_t) * (size_t)V);
+    char *taken = (char *)malloc((size_t)V);
+    if (!lm || !f || !nx || !taken) { free(lm); free(f); free(nx); free(taken); return OR_NOMEM; }
+    int rc = OR_OK;
+    for (int64_t b = 0; b < B && rc == OR_OK; ++b) {
+        rc = score_row(m, states[b], lm, NULL, nx);
+        if (rc) break;
+        const float *row = asr + b * ld;
+        for (int32_t v = 0; v < V; ++v) { f[v] = fmaf(lambda, lm[v], row[v]); taken[v] = 0; }
+        for (int j = 0; j < k; ++j) {
+            int32_t best = -1;
+            for (int32_t v = 0; v < V; ++v)
+                if (!taken[v] && (best < 0 || f[v] > f[best])) best = v;
+            taken[best] = 1;
+            tokens[b * k + j] = best;
+            scores[b * k + j] = f[best];
+            next[b * k + j] = nx[best];
+        }
+    }
+    free(lm); free(f); free(nx); free(taken);
+    return rc;
+}
+
 typedef struct {
     const oracle_model *m;
     const float *asr;

@@ -31,6 +31,7 @@ ERROR_NAMES = {
 EXPORTED = [
     "ngpu_lm_build", "ngpu_lm_free", "ngpu_lm_info", "ngpu_lm_state_context", "ngpu_lm_device_bytes",
     "ngpu_lm_upload", "ngpu_lm_advance", "ngpu_lm_fused_greedy_step", "ngpu_lm_fused_greedy_decode",
+    "ngpu_lm_fused_topk",
     "ngpu_lm_check_states",
     "ngpu_lm_query_bytes", "ngpu_lm_host_image", "ngpu_lm_last_error",
 ]
@@ -80,6 +81,7 @@ def load_library(path: str = LIB_PATH):
     lib.ngpu_lm_fused_greedy_step.argtypes = [vp, vp, i64, i64, i32, ctypes.c_float, vp, vp, vp, vp]
     lib.ngpu_lm_fused_greedy_decode.argtypes = [vp, vp, i64, i64, i64, i64, vp, i32, ctypes.c_float,
                                                 vp, vp, vp, vp, vp]
+    lib.ngpu_lm_fused_topk.argtypes = [vp, vp, i64, i64, ctypes.c_float, i32, vp, vp, vp, vp, vp]
     lib.ngpu_lm_check_states.argtypes = [vp, vp, ctypes.POINTER(i64)]
     lib.ngpu_lm_query_bytes.argtypes = [vp, vp, i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ngpu_lm_host_image.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(ctypes.c_size_t)]
@@ -203,6 +205,23 @@ class NgpuLM:
             _dptr(prev, torch.int32, "prev") if prev is not None else None,
             _dptr(tokens, torch.int32, "tokens"), _stream_handle(stream)))
         return tokens
+
+    def fused_topk(self, asr, lam: float, k: int, states, stream=None):
+        """k best fused tokens per hypothesis: (tokens int32, scores fp32, next states int32), each [B, k]."""
+        import torch
+        if asr.dim() != 2 or asr.stride(1) != 1 or asr.dtype != torch.float32 or not asr.is_cuda:
+            raise TypeError("asr must be a float32 [B, ld] device tensor with unit stride in the last dimension")
+        B = asr.shape[0]
+        if states.numel() != B:
+            raise ValueError("states must hold B entries")
+        tok = torch.empty((B, k), dtype=torch.int32, device=asr.device)
+        sc = torch.empty((B, k), dtype=torch.float32, device=asr.device)
+        nx = torch.empty((B, k), dtype=torch.int32, device=asr.device)
+        _check(self._lib.ngpu_lm_fused_topk(self._h, ctypes.c_void_p(asr.data_ptr()), B, asr.stride(0), float(lam),
+                                            int(k), _dptr(states, torch.int32, "states"),
+                                            _dptr(tok, torch.int32, "tokens"), _dptr(sc, torch.float32, "scores"),
+                                            _dptr(nx, torch.int32, "next"), _stream_handle(stream)))
+        return tok, sc, nx
 
     def fused_greedy_decode(self, asr, lam: float, states, prev=None, lengths=None,
                             mode: int = NGPU_FUSION_PLAIN, labels=None, label_states=None, stream=None):

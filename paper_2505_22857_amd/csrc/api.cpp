@@ -17,6 +17,9 @@ hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int6
 hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
                                const int32_t *lengths, int mode, float lambda, int32_t *states, int32_t *prev,
                                int32_t *labels, int32_t *label_states, hipStream_t stream);
+hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
+                             const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
+                             hipStream_t stream);
 }  // namespace ngpu
 
 namespace {
@@ -179,6 +182,26 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
     hipError_t e = ngpu::launch_fused_step(t, d_asr, B, asr_ld, mode, lambda, d_states, d_prev, d_tokens,
                                            static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return hip_fail(e, "fused step launch");
+    return ok();
+}
+
+int ngpu_lm_fused_topk(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t asr_ld, float lambda, int32_t k,
+                       const int32_t *d_states, int32_t *d_tokens, float *d_scores, int32_t *d_next,
+                       void *hip_stream) {
+    if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (B < 0 || B > INT32_MAX) return fail(NGPU_E_INVALID_ARG, "B = %lld out of range", (long long)B);
+    if (k < 1 || k > lm->V || k > NGPU_LM_MAX_TOPK)
+        return fail(NGPU_E_INVALID_ARG, "k = %d outside [1, min(V, %d)]", k, NGPU_LM_MAX_TOPK);
+    if (asr_ld < lm->V) return fail(NGPU_E_INVALID_ARG, "asr_ld %lld < V", (long long)asr_ld);
+    if (!std::isfinite(lambda)) return fail(NGPU_E_INVALID_ARG, "lambda must be finite");
+    if (B == 0) return ok();
+    if (!d_asr || !d_states || !d_tokens || !d_scores || !d_next)
+        return fail(NGPU_E_INVALID_ARG, "null device pointer");
+    const ngpu::DevTrie t = dev_view(lm);
+    hipError_t e = ngpu::launch_fused_topk(t, d_asr, B, asr_ld, lambda, k, d_states, d_tokens, d_scores, d_next,
+                                           static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "fused top-k launch");
     return ok();
 }
 

@@ -158,6 +158,71 @@ __global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const fl
     }
 }
 
+// The k best fused scores of one hypothesis per wavefront (beam-search
+// expansion): the row of fused values fmaf(lambda, lm[v], asr[v]) stays in
+// LDS, and k rounds of the wave argmax each take the best token not yet taken
+// (bit 31 of its next-state slot marks it).  Cost O(k V / 64) per wavefront.
+__global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
+                                                           int64_t ld, float lambda, int k,
+                                                           const int32_t *__restrict__ states,
+                                                           int32_t *__restrict__ tokens, float *__restrict__ scores,
+                                                           int32_t *__restrict__ next) {
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    if (b >= B) return;
+    const int V = t.vocab_size;
+    float *ls = lds;
+    int *ln = reinterpret_cast<int *>(ls + lds_row(V));
+    int32_t *otok = tokens + b * k;
+    float *osc = scores + b * k;
+    int32_t *onx = next + b * k;
+    const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    if (s < 0 || s >= t.num_states) {
+        if (lane == 0) atomicAdd(&t.status[0], 1);
+        for (int j = lane; j < k; j += kWave) {
+            otok[j] = -1;
+            osc[j] = NAN;
+            onx[j] = -1;
+        }
+        return;
+    }
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
+    const float *row = asr + b * ld;
+    for (int v = lane; v < V; v += kWave) {   // each lane rewrites only its own slots
+        float lm;
+        int n;
+        slot_value(h, ls[v], ln[v], lm, n);
+        ls[v] = __builtin_fmaf(lambda, lm, row[v]);
+        ln[v] = n;
+    }
+    for (int j = 0; j < k; ++j) {
+        unsigned long long best = 0;
+        for (int v = lane; v < V; v += kWave) {
+            if (ln[v] >= 0) {
+                const unsigned long long key = argmax_key(ls[v], v);
+                best = key > best ? key : best;
+            }
+        }
+        const int w = argmax_index(wave_max_u64(best));
+        if (lane == 0) {
+            otok[j] = w;
+            osc[j] = ls[w];
+            onx[j] = ln[w];
+            ln[w] = ln[w] | int32_t(0x80000000u);
+        }
+    }
+}
+
+hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
+                             const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
+                             hipStream_t stream) {
+    const size_t lds = 2 * size_t(lds_row(t.vocab_size)) * sizeof(float);
+    hipLaunchKernelGGL(fused_topk_kernel, dim3(unsigned(B)), dim3(kWave), lds, stream, t, asr, B, ld, lambda, k,
+                       states, tokens, scores, next);
+    return hipGetLastError();
+}
+
 template <int HPB, int MODE>
 static hipError_t launch_one(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
                              int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {

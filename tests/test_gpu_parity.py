@@ -392,6 +392,42 @@ def test_fused_strided_asr_rows(dev):
     assert np.array_equal(prev.cpu().numpy(), o_prev)
 
 
+@pytest.mark.parametrize("k", [1, 5, 32])
+def test_fused_topk_cfg2(dev, k):
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    B = 50
+    states = uniform_states(m, B, seed=51 + k)
+    asr = asr_logprobs((B, V), seed=52 + k)
+    asr[:3] = -7.0                            # full ties: lower index first
+    case(f"fused top-k cfg2 B={B} k={k}")
+    tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), 0.6, k, torch.from_numpy(states).to(dev))
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    ot, osc, onx = o.fused_topk(asr, 0.6, k, states)
+    assert np.array_equal(tok.cpu().numpy(), ot)
+    assert np.array_equal(nx.cpu().numpy(), onx)
+    assert np.abs(sc.cpu().numpy() - osc).max() <= TOL
+
+
+def test_fused_topk_odd_vocab_and_bad_state(dev):
+    m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
+    V = m.vocab_size
+    states = uniform_states(m, 9, seed=53)
+    states[4] = -3
+    asr = asr_logprobs((9, V), seed=54)
+    case("fused top-k V=1025 k=7 with a bad state")
+    tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), 1.1, 7, torch.from_numpy(states).to(dev))
+    torch.cuda.synchronize()
+    assert lm.check_states() == 1
+    t, s_, n = tok.cpu().numpy(), sc.cpu().numpy(), nx.cpu().numpy()
+    assert (t[4] == -1).all() and np.isnan(s_[4]).all() and (n[4] == -1).all()
+    good = [0, 1, 2, 3, 5, 6, 7, 8]
+    ot, osc, onx = o.fused_topk(asr[good], 1.1, 7, states[good])
+    assert np.array_equal(t[good], ot) and np.array_equal(n[good], onx)
+    assert np.abs(s_[good] - osc).max() <= TOL
+
+
 def test_fused_out_of_range_state(dev):
     m, lm, o = cfg_pair(1)
     V = m.vocab_size

@@ -333,6 +333,33 @@ def test_ctc_lambda_zero_is_textbook_greedy_ctc(oracle_lib):
         assert adv == collapse(raw[b])
 
 
+def test_topk_reductions(oracle_lib):
+    """k = 1 is the plain greedy step; lambda = 0 is a stable descending sort of the ASR row;
+    k = V lists every token once, fused scores non-increasing."""
+    m = make_config_model(1)
+    o = Oracle.from_model(m)
+    V = m.vocab_size
+    rng = np.random.default_rng(15)
+    states = rng.integers(0, o.num_states, 40).astype(np.int32)
+    asr = asr_logprobs((40, V), seed=16)
+    asr[:4, :] = -2.0                                  # full ties
+    tok, sc, nx = o.fused_topk(asr, 0.7, 1, states)
+    st = states.copy()
+    g = o.greedy_step(asr, MODE_PLAIN, 0.7, st)
+    assert tok[:, 0].tolist() == g.tolist() and nx[:, 0].tolist() == st.tolist()
+    tok, sc, nx = o.fused_topk(asr, 0.0, 9, states)
+    order = np.argsort(-asr, axis=1, kind="stable")[:, :9]
+    assert (tok == order).all()
+    tok, sc, nx = o.fused_topk(asr, 1.3, V, states[:5])
+    for b in range(5):
+        assert sorted(tok[b].tolist()) == list(range(V))
+        assert (np.diff(sc[b]) <= 0).all()
+        s32, n, _ = o.advance(states[b:b + 1])
+        # the fused score is lambda * lm + asr with one rounding
+        assert np.abs(sc[b] - (np.float64(np.float32(1.3)) * s32[0] + asr[b])[tok[b]]).max() < 1e-5
+        assert (nx[b] == n[0][tok[b]]).all()
+
+
 def test_generator_and_oracle_number_states_alike(oracle_lib):
     check_generator_ids(oracle.LIB_PATH)
 

@@ -82,6 +82,16 @@ typedef struct {
     int64_t device_bytes;         /* size of the device image */
 } ngpu_lm_info_t;
 
+/* Build flag: the list also holds the sentence markers of an ARPA model, as
+ * token V (<s>) and token V + 1 (</s>).  <s> may only open an n-gram and is
+ * never scored (its unigram weight is ignored); the state of the context <s>
+ * is the start state (ngpu_lm_start_state).  </s> may only close an n-gram;
+ * n-grams ending in </s> are not arcs but give each state its final weight,
+ * the </s> score folded through the backoff chain at build time (Section 2.3,
+ * AED; ngpu_lm_final_weights, NGPU_FUSION_AED).  Both need a unigram (or, for
+ * </s>, an <unk> weight). */
+#define NGPU_BUILD_BOS_EOS 1u
+
 /* Build the trie from a closed n-gram list (Section 2.2): states numbered
  * canonically, arcs sorted by (from_state, token) with one contiguous range per
  * state, a dense row over all V tokens for the empty context (a token without a
@@ -89,8 +99,9 @@ typedef struct {
  * a unigram), and per state its backoff weight and backoff state (its context
  * minus the first token).  An arc of order < N leads to the state of its own
  * n-gram, an arc of order N to the state of its last N-1 tokens.
- * vocab_size: 1..NGPU_LM_MAX_VOCAB; additionally ceil(log2 V) * N <= 128.
- * flags: must be 0.  The list is read only during the call.
+ * vocab_size: 1..NGPU_LM_MAX_VOCAB; additionally ceil(log2 V') * N <= 128 with
+ * V' = V (V + 2 with NGPU_BUILD_BOS_EOS).
+ * flags: 0 or NGPU_BUILD_BOS_EOS.  The list is read only during the call.
  * On success *out holds a new handle (free with ngpu_lm_free). */
 int ngpu_lm_build(const ngpu_ngram_list *list, int32_t vocab_size, float unk_logprob,
                   uint32_t flags, ngpu_lm **out);
@@ -102,6 +113,18 @@ int ngpu_lm_info(const ngpu_lm *lm, ngpu_lm_info_t *out);
 /* Context tuple of a state: writes its order to *order_out (0 for state 0) and
  * its tokens to tokens_out[0 .. order-1] (capacity max_order - 1). */
 int ngpu_lm_state_context(const ngpu_lm *lm, int64_t state, int32_t *tokens_out, int32_t *order_out);
+
+/* The state decoding starts from: the context <s> for a model built with
+ * NGPU_BUILD_BOS_EOS (and order >= 2), else the empty context 0. */
+int ngpu_lm_start_state(const ngpu_lm *lm, int64_t *state);
+
+/* Final weight of each state d_states[b] into d_final[b] (fp32): the </s>
+ * score of the state (Section 2.3, AED), precomputed per state at build time
+ * by the same fp32 fold as a query.  Needs NGPU_BUILD_BOS_EOS
+ * (NGPU_E_INVALID_ARG otherwise).  Out-of-range states give NaN and are
+ * counted for ngpu_lm_check_states.  Asynchronous on hip_stream. */
+int ngpu_lm_final_weights(const ngpu_lm *lm, const int32_t *d_states, int64_t B, float *d_final,
+                          void *hip_stream);
 
 /* Bytes of device memory the trie image needs (also in ngpu_lm_info). */
 size_t ngpu_lm_device_bytes(const ngpu_lm *lm);
@@ -129,13 +152,14 @@ int ngpu_lm_advance(const ngpu_lm *lm, const int32_t *d_states, int64_t B, float
 enum ngpu_fusion_mode {
     NGPU_FUSION_PLAIN = 0,        /* argmax_v fma(lambda, lm[v], asr[v]) over v < V, then advance */
     NGPU_FUSION_CTC = 1,          /* blank / repeat / other groups (Section 2.3, CTC) */
-    NGPU_FUSION_TRANSDUCER = 2    /* two-stage selection (Section 2.3, transducers) */
+    NGPU_FUSION_TRANSDUCER = 2,   /* two-stage selection (Section 2.3, transducers) */
+    NGPU_FUSION_AED = 3           /* class V is <eos>, scored with the state's final weight (Section 2.3, AED) */
 };
 
 /* One greedy shallow-fusion step (Section 2.3) for B hypotheses.
  * d_asr: [B, asr_ld] fp32 ASR log-probabilities; row b holds classes 0..V-1
- *   (tokens) and, for CTC and transducer modes, class V = blank; asr_ld >= V
- *   (PLAIN) or >= V + 1.
+ *   (tokens) and, for CTC and transducer modes, class V = blank (AED: <eos>);
+ *   asr_ld >= V (PLAIN) or >= V + 1.
  * lambda: LM weight; the fused score of token v is fmaf(lambda, lm[v], asr[v])
  *   (single rounding), lm[v] being the advance score.
  * PLAIN: label = argmax over v < V of the fused score; state <- next[label].
@@ -145,6 +169,9 @@ enum ngpu_fusion_mode {
  *   of the fused score, and state <- next[label].  Then d_prev[b] = label.
  * TRANSDUCER: a = raw argmax over V + 1 classes; blank stays blank with no state
  *   change; otherwise label = fused argmax over v < V and the state advances.
+ * AED (model built with NGPU_BUILD_BOS_EOS): class V is <eos>; label = argmax
+ *   over v <= V of the fused score, <eos> using the state's final weight as its
+ *   LM score; <eos> leaves the state unchanged, a token advances it.
  * Ties go to the lowest index.  In/out: d_states[B] (int32), d_prev[B] (CTC
  * only; may be NULL otherwise).  Out: d_tokens[B] (int32 label, V = blank).
  * Out-of-range states give label -1, leave the state unchanged and are counted

@@ -15,7 +15,7 @@ import subprocess
 
 import numpy as np
 
-MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER = 0, 1, 2
+MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER, MODE_AED = 0, 1, 2, 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
@@ -45,7 +45,11 @@ def load(path: str = LIB_PATH):
     i32p = ctypes.POINTER(ctypes.c_int32)
     vp = ctypes.c_void_p
     lib.oracle_create.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, vp, vp, vp, vp,
-                                  ctypes.c_float, ctypes.POINTER(vp)]
+                                  ctypes.c_float, ctypes.c_int, ctypes.POINTER(vp)]
+    lib.oracle_final.argtypes = [vp, vp, ctypes.c_int64, vp]
+    lib.oracle_final.restype = ctypes.c_int
+    lib.oracle_start_state.argtypes = [vp]
+    lib.oracle_start_state.restype = ctypes.c_int64
     lib.oracle_create.restype = ctypes.c_int
     lib.oracle_free.argtypes = [vp]
     lib.oracle_num_states.argtypes = [vp]
@@ -84,7 +88,7 @@ class Oracle:
     """The oracle over an n-gram list (natural-log fp32 weights)."""
 
     def __init__(self, vocab_size, max_order, order, tokens, logprob, backoff,
-                 unk_logprob=float("nan"), lib_path: str = LIB_PATH):
+                 unk_logprob=float("nan"), lib_path: str = LIB_PATH, bos_eos: bool = False):
         self._lib = load(lib_path)
         self.V = int(vocab_size)
         self.N = int(max_order)
@@ -94,7 +98,8 @@ class Oracle:
         backoff = np.ascontiguousarray(backoff, np.float32)
         h = ctypes.c_void_p()
         rc = self._lib.oracle_create(self.V, self.N, len(order), _ptr(order), _ptr(tokens),
-                                     _ptr(logprob), _ptr(backoff), float(unk_logprob), ctypes.byref(h))
+                                     _ptr(logprob), _ptr(backoff), float(unk_logprob), int(bool(bos_eos)),
+                                     ctypes.byref(h))
         if rc != 0:
             raise OracleError(rc, self._lib.oracle_last_error().decode())
         self._h = h
@@ -103,7 +108,7 @@ class Oracle:
     def from_model(cls, model, lib_path: str = LIB_PATH, shuffle_seed=None):
         order, tokens, logprob, backoff = model.to_list(shuffle_seed)
         return cls(model.vocab_size, model.max_order, order, tokens, logprob, backoff,
-                   model.unk_logprob, lib_path)
+                   model.unk_logprob, lib_path, bos_eos=getattr(model, "bos_eos", False))
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -126,6 +131,19 @@ class Oracle:
         ctx = list(ctx)
         buf = (ctypes.c_int32 * max(1, len(ctx)))(*ctx)
         return int(self._lib.oracle_state_of(self._h, buf, len(ctx)))
+
+    @property
+    def start_state(self) -> int:
+        return int(self._lib.oracle_start_state(self._h))
+
+    def final(self, states):
+        """The </s> score of each state (models with <s>/</s>)."""
+        states = np.ascontiguousarray(states, np.int32)
+        out = np.empty(len(states), np.float32)
+        rc = self._lib.oracle_final(self._h, _ptr(states), len(states), _ptr(out))
+        if rc != 0:
+            raise OracleError(rc, "final")
+        return out
 
     def advance(self, states, nthreads: int = 1, want64: bool = False):
         """Rows for a batch of states: (scores fp32 [B,V], next int32 [B,V], scores double or None)."""
@@ -194,4 +212,4 @@ class Oracle:
 
 
 __all__ = ["Oracle", "OracleError", "build", "load",
-           "MODE_PLAIN", "MODE_CTC", "MODE_TRANSDUCER", "LIB_PATH", "SRC_PATH"]
+           "MODE_PLAIN", "MODE_CTC", "MODE_TRANSDUCER", "MODE_AED", "LIB_PATH", "SRC_PATH"]

@@ -18,10 +18,11 @@ from typing import Dict, Tuple
 
 class BruteForce:
     def __init__(self, vocab_size, max_order, order, tokens, logprob, backoff,
-                 unk_logprob=float("nan")):
+                 unk_logprob=float("nan"), eos=None):
         self.V = int(vocab_size)
         self.N = int(max_order)
         self.unk = float(unk_logprob)
+        self.eos = eos              # id of </s>: n-grams ending in it are no contexts
         self.W: Dict[Tuple[int, ...], float] = {}
         self.B: Dict[Tuple[int, ...], float] = {}
         for i in range(len(order)):
@@ -31,7 +32,8 @@ class BruteForce:
 
     @classmethod
     def from_model(cls, model):
-        return cls(model.vocab_size, model.max_order, *model.to_list(), model.unk_logprob)
+        eos = model.vocab_size + 1 if getattr(model, "bos_eos", False) else None
+        return cls(model.vocab_size, model.max_order, *model.to_list(), model.unk_logprob, eos=eos)
 
     def _rec(self, ctx: Tuple[int, ...], v: int) -> float:
         if ctx + (v,) in self.W:
@@ -48,6 +50,8 @@ class BruteForce:
         return self._rec(ctx, int(v))
 
     def is_context(self, c: Tuple[int, ...]) -> bool:
+        if len(c) and self.eos is not None and c[-1] == self.eos:
+            return False
         return len(c) == 0 or (len(c) < self.N and c in self.W)
 
     def state_context(self, history) -> Tuple[int, ...]:

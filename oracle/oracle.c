@@ -29,7 +29,9 @@
  *                previous label unchanged without rescoring, otherwise it
  *                takes the fused argmax over the other tokens (not blank, not
  *                the previous label) and advances; the transducer mode keeps
- *                blank, otherwise takes the fused argmax over all V tokens.
+ *                blank, otherwise takes the fused argmax over all V tokens;
+ *                the AED mode adds class V = <eos>, scored with the LM's
+ *                </s> weight of the state, and keeps the state when it wins.
  *                Ties go to the lowest index (strict '>' scan).
  *
  * Parity pins (no external implementation exists): hand-derived values on the
@@ -72,7 +74,8 @@ typedef struct {
     int64_t *slot;  /* row index or -1 */
     int64_t S;
     int64_t *state_row; /* [S], state_row[0] = -1 (empty context) */
-    int64_t *row_state; /* [M], -1 for highest-order n-grams */
+    int64_t *row_state; /* [M], -1 for n-grams that are no context */
+    int special;        /* token V is <s>, token V + 1 is </s> */
 } oracle_model;
 
 static char g_err[256];
@@ -126,14 +129,17 @@ void oracle_free(oracle_model *m) {
     free(m);
 }
 
+/* flags & 1: the list uses token V for <s> and V + 1 for </s>.  A context
+ * (state) is a listed n-gram of order < N that does not end in </s>. */
 int oracle_create(int32_t V, int32_t N, int64_t M, const int32_t *order, const int32_t *tokens,
-                  const float *logprob, const float *backoff, float unk_logprob,
+                  const float *logprob, const float *backoff, float unk_logprob, int flags,
                   oracle_model **out) {
     *out = NULL;
     if (V <= 0 || N < 1 || N > ORACLE_MAX_ORDER || M < 0) { set_err("bad sizes"); return OR_BAD_ARG; }
     oracle_model *m = (oracle_model *)calloc(1, sizeof *m);
     if (!m) return OR_NOMEM;
     m->V = V; m->N = N; m->M = M;
+    m->special = flags & 1;
     m->unk = unk_logprob;
     m->has_unk = !isnan(unk_logprob);
     m->ord = (int32_t *)malloc(sizeof(int32_t) * (size_t)(M ? M : 1));
@@ -158,15 +164,16 @@ int oracle_create(int32_t V, int32_t N, int64_t M, const int32_t *order, const i
         int k = m->ord[r];
         if (k < 1 || k > N) { oracle_free(m); set_err("order out of range"); return OR_ORDER; }
         const int32_t *t = m->tok + r * N;
+        const int32_t vt = m->special ? V + 2 : V;
         for (int i = 0; i < k; ++i)
-            if (t[i] < 0 || t[i] >= V) { oracle_free(m); set_err("token out of range"); return OR_TOKEN; }
+            if (t[i] < 0 || t[i] >= vt) { oracle_free(m); set_err("token out of range"); return OR_TOKEN; }
         uint64_t mask = (uint64_t)m->cap - 1, i = hash_tuple(t, k) & mask;
         while (m->slot[i] >= 0) {
             if (same_tuple(m, m->slot[i], t, k)) { oracle_free(m); set_err("duplicate n-gram"); return OR_DUP; }
             i = (i + 1) & mask;
         }
         m->slot[i] = r;
-        if (k < N) ++n_states;
+        if (k < N && !(m->special && t[k - 1] == V + 1)) ++n_states;
     }
     if (!m->has_unk) {
         for (int32_t v = 0; v < V; ++v)
@@ -179,7 +186,7 @@ int oracle_create(int32_t V, int32_t N, int64_t M, const int32_t *order, const i
     m->state_row[0] = -1;
     int64_t j = 1;
     for (int64_t r = 0; r < M; ++r)
-        if (m->ord[r] < N) m->state_row[j++] = r;
+        if (m->ord[r] < N && !(m->special && m->tok[r * N + m->ord[r] - 1] == V + 1)) m->state_row[j++] = r;
     qsort_r(m->state_row + 1, (size_t)(n_states - 1), sizeof(int64_t), cmp_state, m);
     for (int64_t r = 0; r < M; ++r) m->row_state[r] = -1;
     for (int64_t s = 1; s < n_states; ++s) m->row_state[m->state_row[s]] = s;
@@ -256,6 +263,28 @@ static int score_row(const oracle_model *m, int64_t s, float *s32, double *s64, 
     return OR_OK;
 }
 
+/* The </s> score of each state (Section 2.3, AED: the final weight), from
+ * the same rule as any token; needs a model with <s>/</s>. */
+int oracle_final(const oracle_model *m, const int32_t *states, int64_t B, float *out) {
+    if (!m->special) return OR_BAD_ARG;
+    int32_t c[ORACLE_MAX_ORDER], nx;
+    double d;
+    for (int64_t b = 0; b < B; ++b) {
+        int n = oracle_state_context(m, states[b], c);
+        if (n < 0) return OR_BAD_STATE;
+        score_one(m, c, n, m->V + 1, &out[b], &d, &nx);
+    }
+    return OR_OK;
+}
+
+/* The state of the context <s> (0 without <s>/</s>). */
+int64_t oracle_start_state(const oracle_model *m) {
+    if (!m->special) return 0;
+    int32_t bos = m->V;
+    int64_t s = oracle_state_of(m, &bos, 1);
+    return s < 0 ? 0 : s;
+}
+
 typedef struct {
     const oracle_model *m;
     const int32_t *states;
@@ -309,7 +338,7 @@ int oracle_advance(const oracle_model *m, const int32_t *states, int64_t B, floa
     return OR_OK;
 }
 
-enum { MODE_PLAIN = 0, MODE_CTC = 1, MODE_TRANSDUCER = 2 };
+enum { MODE_PLAIN = 0, MODE_CTC = 1, MODE_TRANSDUCER = 2, MODE_AED = 3 };
 
 /* One greedy step for one hypothesis.  asr has V+1 entries for CTC/transducer
  * (blank = V) and at least V for plain fusion.  Returns the label. */
@@ -333,6 +362,12 @@ static int32_t greedy_one(const oracle_model *m, const float *asr, int mode, flo
         float f = fmaf(lambda, lm[v], asr[v]);
         if (best < 0 || f > bestval) { best = v; bestval = f; }
     }
+    if (mode == MODE_AED) {   /* class V is <eos>: the LM's </s> score of the state */
+        float fin;
+        oracle_final(m, state, 1, &fin);
+        float f = fmaf(lambda, fin, asr[V]);
+        if (f > bestval) return V;   /* sentence ends: the state stays */
+    }
     *state = nx[best];
     if (mode == MODE_CTC) *prev = best;
     return best;
@@ -341,7 +376,7 @@ static int32_t greedy_one(const oracle_model *m, const float *asr, int mode, flo
 /* One fused step over B hypotheses (in-place states/prev). */
 int oracle_greedy_step(const oracle_model *m, const float *asr, int64_t B, int64_t ld, int mode,
                        float lambda, int32_t *states, int32_t *prev, int32_t *tokens_out) {
-    if (mode < 0 || mode > 2) return OR_BAD_ARG;
+    if (mode < 0 || mode > 3 || (mode == MODE_AED && !m->special)) return OR_BAD_ARG;
     float *lm = (float *)malloc(sizeof(float) * (size_t)m->V);
     int32_t *nx = (int32_t *)malloc(sizeof(int32_t) * (size_t)m->V);
     if (!lm || !nx) { free(lm); free(nx); return OR_NOMEM; }
@@ -428,7 +463,7 @@ static void *dec_worker(void *p) {
 int oracle_decode(const oracle_model *m, const float *asr, int64_t B, int64_t T, int64_t ld, int mode,
                   float lambda, const int32_t *starts, const int32_t *lengths, const int32_t *prev0,
                   int32_t *labels, int32_t *states_out, int nthreads) {
-    if (mode < 0 || mode > 2) return OR_BAD_ARG;
+    if (mode < 0 || mode > 3 || (mode == MODE_AED && !m->special)) return OR_BAD_ARG;
     nthreads = clamp_threads(nthreads, B);
     dec_job jobs[256];
     for (int t = 0; t < nthreads; ++t) {

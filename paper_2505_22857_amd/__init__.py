@@ -18,7 +18,8 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libngpu_lm.so")
 
-NGPU_FUSION_PLAIN, NGPU_FUSION_CTC, NGPU_FUSION_TRANSDUCER = 0, 1, 2
+NGPU_FUSION_PLAIN, NGPU_FUSION_CTC, NGPU_FUSION_TRANSDUCER, NGPU_FUSION_AED = 0, 1, 2, 3
+NGPU_BUILD_BOS_EOS = 1
 MAX_ORDER = 10
 MAX_VOCAB = 8192
 
@@ -31,7 +32,7 @@ ERROR_NAMES = {
 EXPORTED = [
     "ngpu_lm_build", "ngpu_lm_free", "ngpu_lm_info", "ngpu_lm_state_context", "ngpu_lm_device_bytes",
     "ngpu_lm_upload", "ngpu_lm_advance", "ngpu_lm_fused_greedy_step", "ngpu_lm_fused_greedy_decode",
-    "ngpu_lm_fused_topk",
+    "ngpu_lm_fused_topk", "ngpu_lm_start_state", "ngpu_lm_final_weights",
     "ngpu_lm_check_states",
     "ngpu_lm_query_bytes", "ngpu_lm_host_image", "ngpu_lm_last_error",
 ]
@@ -81,6 +82,8 @@ def load_library(path: str = LIB_PATH):
     lib.ngpu_lm_fused_greedy_step.argtypes = [vp, vp, i64, i64, i32, ctypes.c_float, vp, vp, vp, vp]
     lib.ngpu_lm_fused_greedy_decode.argtypes = [vp, vp, i64, i64, i64, i64, vp, i32, ctypes.c_float,
                                                 vp, vp, vp, vp, vp]
+    lib.ngpu_lm_start_state.argtypes = [vp, ctypes.POINTER(i64)]
+    lib.ngpu_lm_final_weights.argtypes = [vp, vp, i64, vp, vp]
     lib.ngpu_lm_fused_topk.argtypes = [vp, vp, i64, i64, ctypes.c_float, i32, vp, vp, vp, vp, vp]
     lib.ngpu_lm_check_states.argtypes = [vp, vp, ctypes.POINTER(i64)]
     lib.ngpu_lm_query_bytes.argtypes = [vp, vp, i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -119,7 +122,7 @@ class NgpuLM:
     """A trie built from an n-gram list (natural-log fp32 weights)."""
 
     def __init__(self, vocab_size: int, max_order: int, order, tokens, logprob, backoff,
-                 unk_logprob: float = float("nan")):
+                 unk_logprob: float = float("nan"), bos_eos: bool = False):
         self._lib = load_library()
         self._h = None
         order = np.ascontiguousarray(order, np.int32)
@@ -129,8 +132,8 @@ class NgpuLM:
         lst = _NgramList(len(order), int(max_order), order.ctypes.data, tokens.ctypes.data,
                          logprob.ctypes.data, backoff.ctypes.data)
         h = ctypes.c_void_p()
-        _check(self._lib.ngpu_lm_build(ctypes.byref(lst), int(vocab_size), float(unk_logprob), 0,
-                                       ctypes.byref(h)))
+        _check(self._lib.ngpu_lm_build(ctypes.byref(lst), int(vocab_size), float(unk_logprob),
+                                       NGPU_BUILD_BOS_EOS if bos_eos else 0, ctypes.byref(h)))
         self._h = h
         info = _Info()
         _check(self._lib.ngpu_lm_info(h, ctypes.byref(info)))
@@ -139,11 +142,16 @@ class NgpuLM:
         self.max_order = int(info.max_order)
         self.vocab_size = int(info.vocab_size)
         self.device_bytes = int(info.device_bytes)
+        self.bos_eos = bool(bos_eos)
+        st = ctypes.c_int64()
+        _check(self._lib.ngpu_lm_start_state(h, ctypes.byref(st)))
+        self.start_state = int(st.value)
         self._dev = None
 
     @classmethod
     def from_model(cls, model, shuffle_seed: Optional[int] = None):
-        return cls(model.vocab_size, model.max_order, *model.to_list(shuffle_seed), model.unk_logprob)
+        return cls(model.vocab_size, model.max_order, *model.to_list(shuffle_seed), model.unk_logprob,
+                   bos_eos=getattr(model, "bos_eos", False))
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -205,6 +213,15 @@ class NgpuLM:
             _dptr(prev, torch.int32, "prev") if prev is not None else None,
             _dptr(tokens, torch.int32, "tokens"), _stream_handle(stream)))
         return tokens
+
+    def final_weights(self, states, out=None, stream=None):
+        """fp32 final (</s>) weight of each state of device int32 ``states``."""
+        import torch
+        if out is None:
+            out = torch.empty(states.numel(), dtype=torch.float32, device=states.device)
+        _check(self._lib.ngpu_lm_final_weights(self._h, _dptr(states, torch.int32, "states"), states.numel(),
+                                               _dptr(out, torch.float32, "out"), _stream_handle(stream)))
+        return out
 
     def fused_topk(self, asr, lam: float, k: int, states, stream=None):
         """k best fused tokens per hypothesis: (tokens int32, scores fp32, next states int32), each [B, k]."""
@@ -275,5 +292,5 @@ class NgpuLM:
         return int(hbm.value), int(tot.value)
 
 
-__all__ = ["NgpuLM", "NgpuError", "load_library", "LIB_PATH", "EXPORTED",
-           "NGPU_FUSION_PLAIN", "NGPU_FUSION_CTC", "NGPU_FUSION_TRANSDUCER"]
+__all__ = ["NgpuLM", "NgpuError", "load_library", "LIB_PATH", "EXPORTED", "NGPU_BUILD_BOS_EOS",
+           "NGPU_FUSION_PLAIN", "NGPU_FUSION_CTC", "NGPU_FUSION_TRANSDUCER", "NGPU_FUSION_AED"]

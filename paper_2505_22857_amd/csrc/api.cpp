@@ -17,6 +17,7 @@ hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int6
 hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
                                const int32_t *lengths, int mode, float lambda, int32_t *states, int32_t *prev,
                                int32_t *labels, int32_t *label_states, hipStream_t stream);
+hipError_t launch_final_weights(const DevTrie &t, const int32_t *states, int64_t B, float *out, hipStream_t stream);
 hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
                              const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
                              hipStream_t stream);
@@ -59,6 +60,7 @@ ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     t.arc_tok = reinterpret_cast<const int32_t *>(base + h.off_arc_tok);
     t.arc_w = reinterpret_cast<const float *>(base + h.off_arc_w);
     t.arc_to = reinterpret_cast<const int32_t *>(base + h.off_arc_to);
+    t.final_w = h.has_final ? reinterpret_cast<const float *>(base + h.off_final) : nullptr;
     t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + h.off_status);
     t.num_states = int32_t(lm->S);
     t.vocab_size = lm->V;
@@ -80,13 +82,13 @@ int ngpu_lm_build(const ngpu_ngram_list *list, int32_t vocab_size, float unk_log
     if (!out) return fail(NGPU_E_INVALID_ARG, "out is null");
     *out = nullptr;
     if (!list) return fail(NGPU_E_INVALID_ARG, "list is null");
-    if (flags != 0) return fail(NGPU_E_INVALID_ARG, "flags must be 0");
+    if ((flags & ~NGPU_BUILD_BOS_EOS) != 0) return fail(NGPU_E_INVALID_ARG, "unknown build flags");
     ngpu_lm *lm = new (std::nothrow) ngpu_lm();
     if (!lm) return fail(NGPU_E_NO_MEMORY, "handle allocation failed");
     std::string err;
     int rc;
     try {
-        rc = ngpu::build_trie(list, vocab_size, unk_logprob, lm, &err);
+        rc = ngpu::build_trie(list, vocab_size, unk_logprob, flags, lm, &err);
     } catch (const std::bad_alloc &) {
         rc = NGPU_E_NO_MEMORY;
         err = "host allocation failed while building the trie";
@@ -128,6 +130,26 @@ int ngpu_lm_state_context(const ngpu_lm *lm, int64_t state, int32_t *tokens_out,
 
 size_t ngpu_lm_device_bytes(const ngpu_lm *lm) { return lm ? lm->image.size() : 0; }
 
+int ngpu_lm_start_state(const ngpu_lm *lm, int64_t *state) {
+    if (!lm || !state) return fail(NGPU_E_INVALID_ARG, "null argument");
+    *state = lm->hdr.start_state;
+    return ok();
+}
+
+int ngpu_lm_final_weights(const ngpu_lm *lm, const int32_t *d_states, int64_t B, float *d_final,
+                          void *hip_stream) {
+    if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
+    if (!lm->hdr.has_final) return fail(NGPU_E_INVALID_ARG, "the model has no </s> (build with NGPU_BUILD_BOS_EOS)");
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld out of range", (long long)B);
+    if (B == 0) return ok();
+    if (!d_states || !d_final) return fail(NGPU_E_INVALID_ARG, "null device pointer");
+    hipError_t e = ngpu::launch_final_weights(dev_view(lm), d_states, B, d_final,
+                                              static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return hip_fail(e, "final weights launch");
+    return ok();
+}
+
 int ngpu_lm_upload(ngpu_lm *lm, void *dev_buf, size_t dev_bytes, void *hip_stream) {
     if (!lm || !dev_buf) return fail(NGPU_E_INVALID_ARG, "null argument");
     if (reinterpret_cast<uintptr_t>(dev_buf) % ngpu::kAlign != 0)
@@ -168,8 +190,10 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
                               void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
     if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
-    if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_TRANSDUCER)
+    if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_AED)
         return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
+    if (mode == NGPU_FUSION_AED && !lm->hdr.has_final)
+        return fail(NGPU_E_INVALID_ARG, "AED fusion needs a model with </s> (NGPU_BUILD_BOS_EOS)");
     if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld outside [0, %lld]", (long long)B,
                                             (long long)kMaxBatch);
     const int64_t need = mode == NGPU_FUSION_PLAIN ? lm->V : int64_t(lm->V) + 1;
@@ -211,8 +235,10 @@ int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B
                                 void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
     if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
-    if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_TRANSDUCER)
+    if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_AED)
         return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
+    if (mode == NGPU_FUSION_AED && !lm->hdr.has_final)
+        return fail(NGPU_E_INVALID_ARG, "AED fusion needs a model with </s> (NGPU_BUILD_BOS_EOS)");
     if (B < 0 || B > INT32_MAX || T < 0) return fail(NGPU_E_INVALID_ARG, "bad sizes B=%lld T=%lld", (long long)B,
                                                      (long long)T);
     if (stride_b < 0 || stride_t < 0) return fail(NGPU_E_INVALID_ARG, "negative strides");

@@ -14,13 +14,16 @@
 // The decode kernel keeps each utterance's state and previous label in
 // registers across frames: frame t + 1 depends on frame t only through them,
 // so a single launch replaces T launches and their host round trips.
+//
+// AED mode (Section 2.3): class V is <eos>, whose LM score is the state's
+// final weight (the </s> score, precomputed per state); <eos> keeps the state.
 #include <hip/hip_runtime.h>
 
 #include "walk.h"
 
 namespace ngpu {
 
-enum { kPlain = 0, kCtc = 1, kTransducer = 2 };
+enum { kPlain = 0, kCtc = 1, kTransducer = 2, kAed = 3 };
 
 // One fused greedy step of the wavefront's hypothesis on ASR row `row`.
 // s: valid state (uniform); pv: previous label (CTC).  Returns the label and
@@ -30,7 +33,8 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *__rest
                                            int pv, float *ls, int *ln, int lane, const float *pf_src = nullptr,
                                            float *pf_dst = nullptr, int pf_n = 0) {
     const int V = t.vocab_size;
-    if (MODE != kPlain) {
+    const float fin = MODE == kAed ? t.final_w[s] : 0.0f;   // <eos> takes the state's final weight
+    if (MODE == kCtc || MODE == kTransducer) {
         unsigned long long best = 0;
         for (int v = lane; v <= V; v += kWave) {
             const unsigned long long k = argmax_key(row[v], v);
@@ -53,7 +57,12 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *__rest
         const unsigned long long k = argmax_key(f, v);
         best = k > best ? k : best;
     }
-    const int w = argmax_index(wave_max_u64(best));
+    best = wave_max_u64(best);
+    if (MODE == kAed) {
+        const unsigned long long ke = argmax_key(__builtin_fmaf(lambda, fin, row[V]), V);
+        if (ke > best) return V;   // <eos>: the sentence ends, the state stays
+    }
+    const int w = argmax_index(best);
     float lm;
     int n;
     slot_value(h, ls[w], ln[w], lm, n);   // uniform w: every lane reads the same slot
@@ -214,6 +223,25 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     }
 }
 
+__global__ __launch_bounds__(256) void final_weights_kernel(DevTrie t, const int32_t *__restrict__ states, int64_t B,
+                                                          float *__restrict__ out) {
+    const int64_t b = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (b >= B) return;
+    const int s = states[b];
+    if (s < 0 || s >= t.num_states) {
+        atomicAdd(&t.status[0], 1);
+        out[b] = NAN;
+        return;
+    }
+    out[b] = t.final_w[s];
+}
+
+hipError_t launch_final_weights(const DevTrie &t, const int32_t *states, int64_t B, float *out, hipStream_t stream) {
+    hipLaunchKernelGGL(final_weights_kernel, dim3(unsigned((B + 255) / 256)), dim3(256), 0, stream, t, states, B,
+                       out);
+    return hipGetLastError();
+}
+
 hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
                              const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
                              hipStream_t stream) {
@@ -240,6 +268,7 @@ hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int6
     switch (mode) {
         case kPlain: return launch_one<1, kPlain>(t, asr, B, ld, lambda, states, prev, tokens, stream);
         case kCtc: return launch_one<1, kCtc>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        case kAed: return launch_one<1, kAed>(t, asr, B, ld, lambda, states, prev, tokens, stream);
         default: return launch_one<1, kTransducer>(t, asr, B, ld, lambda, states, prev, tokens, stream);
     }
 }
@@ -264,6 +293,9 @@ hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, in
                                               label_states, stream);
         case kCtc:
             return launch_decode_mode<kCtc>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                            label_states, stream);
+        case kAed:
+            return launch_decode_mode<kAed>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
                                             label_states, stream);
         default:
             return launch_decode_mode<kTransducer>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,

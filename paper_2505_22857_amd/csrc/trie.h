@@ -23,6 +23,9 @@
 //   arc_tok  int32 [A3]  arcs of states of order >= 2 (n-grams of order >= 3),
 //   arc_w    float [A3]  sorted by (from_state, token) (Section 2.2)
 //   arc_to   int32 [A3]
+//   final    float [S]   with </s> in the model: each state's end-of-sentence
+//                        weight, folded through its backoff chain at build
+//                        time (Section 2.3, AED)
 #pragma once
 
 #include <cstddef>
@@ -50,6 +53,9 @@ struct ImageHeader {
     uint64_t total_bytes;
     int32_t first[NGPU_LM_MAX_ORDER + 1];       // first state id of each order; first[N] = S
     uint64_t off_order[NGPU_LM_MAX_ORDER];      // chain offset (from the chain section) per order
+    uint64_t off_final;                         // final weights float[S] (0 when the model has no </s>)
+    int32_t start_state;                        // state of the context <s> (0 without <s>)
+    int32_t has_final;
 };
 
 struct ChainHead {
@@ -82,6 +88,7 @@ struct DevTrie {
     const int32_t *arc_tok;
     const float *arc_w;
     const int32_t *arc_to;
+    const float *final_w;   // nullptr without </s>
     int32_t *status;
     int32_t num_states;
     int32_t vocab_size;
@@ -109,5 +116,5 @@ struct ngpu_lm {
 
 namespace ngpu {
 // trie_build.cpp
-int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, std::string *err);
+int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags, ngpu_lm *lm, std::string *err);
 }  // namespace ngpu

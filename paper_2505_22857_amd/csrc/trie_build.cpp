@@ -60,9 +60,13 @@ std::string tuple_text(u128 key, int k, int bits) {
 
 }  // namespace
 
-int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, std::string *err) {
+int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags, ngpu_lm *lm, std::string *err) {
     const int N = list->max_order;
     const int64_t M = list->num_ngrams;
+    // with <s> and </s>: token V is <s> (only first), V + 1 is </s> (only last)
+    const bool special = (flags & NGPU_BUILD_BOS_EOS) != 0;
+    const int32_t bos = V, eos = V + 1;
+    const int32_t Vt = special ? V + 2 : V;
     if (N < 1 || N > NGPU_LM_MAX_ORDER) {
         *err = "max_order must be in [1, " + std::to_string(NGPU_LM_MAX_ORDER) + "]";
         return NGPU_E_ORDER_RANGE;
@@ -71,7 +75,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
         *err = "vocab_size must be in [1, " + std::to_string(NGPU_LM_MAX_VOCAB) + "]";
         return NGPU_E_TOO_LARGE;
     }
-    const int bits = bits_for(V);
+    const int bits = bits_for(Vt);
     if (bits * N > 128) {
         *err = "ceil(log2 V) * max_order exceeds 128 bits";
         return NGPU_E_TOO_LARGE;
@@ -102,22 +106,35 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
     }
     std::vector<std::vector<Entry>> ent(N + 1);
     for (int k = 1; k <= N; ++k) ent[k].reserve(count[k]);
+    struct Final {
+        u128 ctx;
+        int order;   // context order
+        int64_t row;
+    };
+    std::vector<Final> finals;   // n-grams ending in </s>: final weights of their contexts
     for (int64_t i = 0; i < M; ++i) {
         int k = list->order[i];
         const int32_t *t = list->tokens + i * N;
         u128 key = 0;
         for (int j = 0; j < k; ++j) {
-            if (t[j] < 0 || t[j] >= V) {
-                *err = "row " + std::to_string(i) + ": token " + std::to_string(t[j]) + " outside [0, V)";
+            if (t[j] < 0 || t[j] >= Vt) {
+                *err = "row " + std::to_string(i) + ": token " + std::to_string(t[j]) + " outside [0, " +
+                       std::to_string(Vt) + ")";
+                return NGPU_E_TOKEN_RANGE;
+            }
+            if (special && ((t[j] == bos && j != 0) || (t[j] == eos && j != k - 1))) {
+                *err = "row " + std::to_string(i) + ": <s> may only open and </s> only close an n-gram";
                 return NGPU_E_TOKEN_RANGE;
             }
             key = (key << bits) | u128(uint32_t(t[j]));
         }
-        if (!std::isfinite(list->logprob[i]) || (k < N && !std::isfinite(list->backoff[i]))) {
+        const bool ends_eos = special && t[k - 1] == eos;
+        if (!std::isfinite(list->logprob[i]) || (k < N && !ends_eos && !std::isfinite(list->backoff[i]))) {
             *err = "row " + std::to_string(i) + ": non-finite weight";
             return NGPU_E_NONFINITE;
         }
-        ent[k].push_back({key, i});
+        if (ends_eos) finals.push_back({key >> bits, k - 1, i});
+        else ent[k].push_back({key, i});
     }
 
     std::vector<OrderLevel> lv(N + 1);
@@ -139,9 +156,17 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
         }
         std::vector<Entry>().swap(e);
     }
-    if (!has_unk && int64_t(lv[1].key.size()) < V) {
-        *err = "a token has no unigram and no <unk> weight was given";
-        return NGPU_E_MISSING_UNIGRAM;
+    {
+        int64_t regular = 0;   // unigrams of scored tokens (not <s>)
+        for (const u128 &k1 : lv[1].key) regular += k1 < u128(uint32_t(V)) ? 1 : 0;
+        if (!has_unk && regular < V) {
+            *err = "a token has no unigram and no <unk> weight was given";
+            return NGPU_E_MISSING_UNIGRAM;
+        }
+        if (special && find_rank(lv[1].key, u128(uint32_t(bos))) < 0) {
+            *err = "<s> has no unigram, so there is no start state";
+            return NGPU_E_MISSING_UNIGRAM;
+        }
     }
 
     // ---- closure: prefix and suffix of every order-k n-gram are listed
@@ -244,6 +269,11 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
     off = align_up(off + size_t(A3) * 4);
     h.off_arc_to = off;
     off = align_up(off + size_t(A3) * 4);
+    h.has_final = special ? 1 : 0;
+    h.off_final = special ? off : 0;
+    if (special) off = align_up(off + size_t(S) * 4);
+    h.start_state = 0;
+    if (special && N > 1) h.start_state = int32_t(first[1] + find_rank(lv[1].key, u128(uint32_t(bos))));
     h.total_bytes = off;
 
     std::vector<unsigned char> img;
@@ -268,6 +298,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
     }
     for (size_t p = 0; p < lv[1].key.size(); ++p) {
         int32_t v = int32_t(uint64_t(lv[1].key[p]));
+        if (v >= V) continue;   // <s> is a context only, never scored
         dense_w[v] = lv[1].w[p];
         dense_to[v] = N > 1 ? int32_t(first[1] + int64_t(p)) : 0;
     }
@@ -350,6 +381,55 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, ngpu_lm *lm, s
             hd.acc0 = acc + rec[s].bw;
             hd.nlev_group = (k - 1) | (row_group[size_t(s)] << 16);
             std::memcpy(r, &hd, sizeof hd);
+        }
+    }
+
+    // final weights: the </s> score of every state, by the same fp32 fold as a
+    // query (the first state on the chain that lists </s> adds its weight)
+    if (special) {
+        std::vector<float> expl(size_t(S), 0.0f);
+        std::vector<char> has(size_t(S), 0);
+        std::sort(finals.begin(), finals.end(), [](const Final &a, const Final &b) {
+            return a.order != b.order ? a.order < b.order : a.ctx < b.ctx;
+        });
+        for (size_t i = 0; i < finals.size(); ++i) {
+            const Final &f = finals[i];
+            if (i && f.order == finals[i - 1].order && f.ctx == finals[i - 1].ctx) {
+                *err = "duplicate </s> n-gram";
+                return NGPU_E_DUPLICATE_NGRAM;
+            }
+            int64_t st = 0;
+            if (f.order > 0) {
+                const int64_t r = find_rank(lv[f.order].key, f.ctx);
+                if (r < 0) {
+                    *err = "an n-gram ending in </s> has no listed context";
+                    return NGPU_E_MISSING_PREFIX;
+                }
+                st = first[f.order] + r;
+            }
+            expl[size_t(st)] = list->logprob[f.row];
+            has[size_t(st)] = 1;
+        }
+        if (!has[0] && !has_unk) {
+            *err = "</s> has no unigram and no <unk> weight was given";
+            return NGPU_E_MISSING_UNIGRAM;
+        }
+        float *fin = reinterpret_cast<float *>(img.data() + h.off_final);
+        for (int64_t s0 = 0; s0 < S; ++s0) {
+            float acc = 0.0f;
+            int64_t x = s0;
+            for (int lvl = 0; lvl <= N; ++lvl) {
+                if (has[size_t(x)]) {
+                    fin[s0] = acc + expl[size_t(x)];
+                    break;
+                }
+                if (x == 0) {
+                    fin[s0] = acc + unk;
+                    break;
+                }
+                acc = acc + rec[size_t(x)].bw;
+                x = rec[size_t(x)].bto;
+            }
         }
     }
 

@@ -63,7 +63,21 @@ class NgramModel:
     levels: List[Level]               # levels[0] is the root placeholder
     unk_logprob: float = float("nan")
     phrases: Optional[List[np.ndarray]] = None
+    bos_eos: bool = False             # token V is <s> (context only), V + 1 is </s> (predicted only)
     _tokens_cache: dict = field(default_factory=dict, repr=False)
+
+    @property
+    def bos(self) -> int:
+        return self.vocab_size
+
+    @property
+    def eos(self) -> int:
+        return self.vocab_size + 1
+
+    def is_state_row(self, k: int) -> np.ndarray:
+        """Rows of level k that are contexts (all of them, except n-grams ending in </s>)."""
+        tok = self.levels[k].tok
+        return tok != self.eos if self.bos_eos else np.ones(len(tok), bool)
 
     @property
     def counts(self) -> List[int]:
@@ -75,13 +89,20 @@ class NgramModel:
 
     @property
     def num_states(self) -> int:
-        """Root plus every listed n-gram of order < N (the highest order has no states)."""
-        return 1 + int(sum(self.counts[: self.max_order - 1]))
+        """Root plus every listed context of order < N (the highest order has no states)."""
+        return 1 + int(sum(int(self.is_state_row(k).sum()) for k in range(1, self.max_order)))
 
     def state_offset(self, k: int) -> int:
         """Canonical id of the first order-k state (k < N): root 0, then by order, then lexicographic."""
         assert 1 <= k < self.max_order
-        return 1 + int(sum(self.counts[: k - 1]))
+        return 1 + int(sum(int(self.is_state_row(j).sum()) for j in range(1, k)))
+
+    @property
+    def start_state(self) -> int:
+        """State of the context <s> (bos_eos models), else the empty context."""
+        if not self.bos_eos or self.max_order < 2:
+            return 0
+        return int(state_ids_of(self, np.array([[self.bos]]))[0])
 
     def level_tokens(self, k: int) -> np.ndarray:
         """[n_k, k] int32 token tuples of level k, in lexicographic order."""
@@ -151,7 +172,11 @@ def state_ids_of(model: NgramModel, tuples: np.ndarray) -> np.ndarray:
     tuples = np.asarray(tuples)
     k = tuples.shape[1]
     rows = lookup_ids(model, tuples)
-    return np.where(rows >= 0, rows + model.state_offset(k), -1).astype(np.int32)
+    ok = model.is_state_row(k)
+    rank = np.cumsum(ok) - 1                     # rank among the level's contexts
+    ids = np.where(rows >= 0, rank[np.maximum(rows, 0)] + model.state_offset(k), -1)
+    ids = np.where((rows >= 0) & ok[np.maximum(rows, 0)], ids, -1)
+    return ids.astype(np.int32)
 
 
 def _zipf_unigrams(V: int, n1: int, s: float, rng: np.random.Generator):
@@ -176,29 +201,37 @@ def _zipf_unigrams(V: int, n1: int, s: float, rng: np.random.Generator):
 
 
 def _select_candidates(prev: Level, grand_n: int, need: int, forced: np.ndarray,
-                       rng: np.random.Generator) -> np.ndarray:
-    """Keys ``c * n_prev + y`` of the chosen order-k n-grams (c: prefix row, y: suffix row)."""
+                       rng: np.random.Generator, ctx_ok: Optional[np.ndarray] = None,
+                       cand_ok: Optional[np.ndarray] = None) -> np.ndarray:
+    """Keys ``c * n_prev + y`` of the chosen order-k n-grams (c: prefix row, y: suffix row).
+
+    ``ctx_ok`` marks the rows that may be extended (contexts), ``cand_ok`` the
+    rows whose last token may be appended (predictable tokens)."""
     n_prev = len(prev.tok)
     nodes = np.arange(grand_n)
     cb = np.searchsorted(prev.pid, nodes, "left")
     ce = np.searchsorted(prev.pid, nodes, "right")
     s = prev.sid
     lens = (ce - cb)[s]
-    total = int(lens.sum())
+    if ctx_ok is not None:
+        lens = np.where(ctx_ok, lens, 0)
     forced = np.unique(forced.astype(np.int64))
     if len(forced) > need:
         raise ValueError("more forced n-grams than the order's count")
-    if total <= need:
-        c_idx = np.repeat(np.arange(n_prev, dtype=np.int64), lens)
-        starts = np.repeat(cb[s], lens)
-        offs = np.arange(total, dtype=np.int64) - np.repeat(np.cumsum(lens) - lens, lens)
-        return np.sort(c_idx * n_prev + starts + offs)
-    if total <= _MATERIALISE_LIMIT:
+    masked = cand_ok is not None and not cand_ok.all()
+    total = int(lens.sum())
+    if masked or total <= _MATERIALISE_LIMIT:
         c_idx = np.repeat(np.arange(n_prev, dtype=np.int64), lens)
         starts = np.repeat(cb[s], lens)
         offs = np.arange(total, dtype=np.int64) - np.repeat(np.cumsum(lens) - lens, lens)
         y = starts + offs
         del starts, offs
+        if masked:
+            keep = cand_ok[y]
+            c_idx, y = c_idx[keep], y[keep]
+            total = len(y)
+        if total <= need:
+            return np.sort(c_idx * n_prev + y)
         keys = c_idx * n_prev + y
         # exponential clocks: smaller log(E) - log w is drawn earlier
         score = np.log(rng.exponential(size=total)) - (prev.cum[c_idx] + prev.W[y].astype(np.float64))
@@ -212,6 +245,8 @@ def _select_candidates(prev: Level, grand_n: int, need: int, forced: np.ndarray,
     cumew = np.concatenate([[0.0], np.cumsum(ew)])
     mass = cumew[ce] - cumew[cb]
     wc = np.exp(prev.cum - prev.cum.max()) * mass[s]
+    if ctx_ok is not None:
+        wc = wc * ctx_ok
     cdf = np.cumsum(wc)
     cdf /= cdf[-1]
     chosen = [forced]
@@ -247,7 +282,7 @@ def _select_candidates(prev: Level, grand_n: int, need: int, forced: np.ndarray,
     raise RuntimeError("candidate sampling did not reach the requested count")
 
 
-def _assign_probabilities(prev: Level, pid: np.ndarray, sid: np.ndarray, V: int,
+def _assign_probabilities(prev: Level, pid: np.ndarray, sid: np.ndarray, n_pred: int,
                           z_low: np.ndarray, rng: np.random.Generator):
     """Weights of the new level; backoff weights and stored mass Z of its contexts.
 
@@ -262,7 +297,7 @@ def _assign_probabilities(prev: Level, pid: np.ndarray, sid: np.ndarray, V: int,
     l = np.bincount(pid, weights=p_low, minlength=n_prev)
     cnt = np.bincount(pid, minlength=n_prev)
     m = rng.uniform(0.5, 0.95, size=n_prev)
-    full = cnt == V
+    full = cnt == n_pred          # every predictable token continues the context
     m[full] = 1.0
     P = m[pid] * raw / gsum[pid]
     W = np.log(P).astype(np.float32)
@@ -278,9 +313,21 @@ def _assign_probabilities(prev: Level, pid: np.ndarray, sid: np.ndarray, V: int,
     return W, Z
 
 
+# The <s> unigram is a context only; its weight (log10 -99 as KenLM writes it)
+# is never scored.
+BOS_LOGPROB = float(np.float32(-99.0 * np.log(10.0)))
+
+
 def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
-                   phrases: Optional[Sequence[Sequence[int]]] = None) -> NgramModel:
-    """Generate a closed, normalised n-gram model with ``counts[k-1]`` n-grams of order k."""
+                   phrases: Optional[Sequence[Sequence[int]]] = None, bos_eos: bool = False,
+                   eos_prob: float = 0.04) -> NgramModel:
+    """Generate a closed, normalised n-gram model with ``counts[k-1]`` n-grams of order k.
+
+    With ``bos_eos``, token V is ``<s>`` (it opens contexts and is never
+    predicted) and V + 1 is ``</s>`` (it is predicted with unigram probability
+    ``eos_prob`` and never extended); every context then sums to one over the V
+    tokens and ``</s>``.  counts[0] counts the unigrams of the V tokens only.
+    """
     N = len(counts)
     if N < 1:
         raise ValueError("need at least one order")
@@ -288,12 +335,25 @@ def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
     root = Level(pid=np.zeros(1, np.int64), tok=np.zeros(1, np.int32), sid=np.zeros(1, np.int64),
                  W=np.zeros(1, np.float32), B=np.zeros(1, np.float32), cum=np.zeros(1))
     toks, p1, unk = _zipf_unigrams(V, int(counts[0]), zipf_s, rng)
-    W1 = np.log(p1).astype(np.float32)
+    n_pred = V
+    if bos_eos:
+        if not np.isnan(unk):
+            raise ValueError("bos_eos models list every token")
+        p1 = p1 * (1.0 - eos_prob)
+        toks = np.concatenate([toks, [V, V + 1]]).astype(np.int32)
+        W1 = np.concatenate([np.log(p1), [BOS_LOGPROB, np.log(eos_prob)]]).astype(np.float32)
+        n_pred = V + 1
+    else:
+        W1 = np.log(p1).astype(np.float32)
     lv1 = Level(pid=np.zeros(len(toks), np.int64), tok=toks, sid=np.zeros(len(toks), np.int64),
                 W=W1, B=np.zeros(len(toks), np.float32), cum=W1.astype(np.float64))
     model = NgramModel(vocab_size=V, max_order=N, levels=[root, lv1], unk_logprob=unk,
-                       phrases=[np.asarray(p, np.int64) for p in phrases] if phrases is not None else None)
-    z_root = float(np.exp(W1.astype(np.float64)).sum())
+                       phrases=[np.asarray(p, np.int64) for p in phrases] if phrases is not None else None,
+                       bos_eos=bos_eos)
+    pred1 = toks != V if bos_eos else np.ones(len(toks), bool)
+    if bos_eos:
+        lv1.cum = np.where(pred1, lv1.cum, np.log(0.05))   # <s> opens contexts as often as a frequent word
+    z_root = float(np.exp(W1.astype(np.float64))[pred1].sum())
     if not np.isnan(unk):
         z_root += (V - len(toks)) * float(np.exp(np.float64(np.float32(unk))))
     z_levels = [np.array([z_root])]                        # Z per context, level by level
@@ -311,7 +371,11 @@ def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
                 if (c < 0).any() or (y < 0).any():
                     raise ValueError("phrase tokens must all be listed unigrams")
                 forced = c * n_prev + y
-        keys = _select_candidates(prev, grand_n, int(counts[k - 1]), forced, rng)
+        ctx_ok = cand_ok = None
+        if bos_eos:
+            ctx_ok = prev.tok != V + 1                     # </s> ends a sentence: no context
+            cand_ok = prev.tok != V                        # <s> is never predicted
+        keys = _select_candidates(prev, grand_n, int(counts[k - 1]), forced, rng, ctx_ok, cand_ok)
         pid = keys // n_prev
         sid = keys % n_prev
         tok = prev.tok[sid]
@@ -319,7 +383,7 @@ def generate_model(V: int, counts: Sequence[int], zipf_s: float, seed: int,
         pid, sid, tok = pid[order], sid[order], tok[order]
         # stored mass of each context's suffix: Z of the level below (the root for unigrams)
         z_low = z_levels[k - 2][prev.sid]
-        W, z_prev = _assign_probabilities(prev, pid, sid, V, z_low, rng)
+        W, z_prev = _assign_probabilities(prev, pid, sid, n_pred, z_low, rng)
         z_levels.append(z_prev)
         cum = prev.cum[pid] + W.astype(np.float64)
         model.levels.append(Level(pid=pid, tok=tok.astype(np.int32), sid=sid, W=W,

@@ -16,7 +16,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 import paper_2505_22857_amd as ng  # noqa: E402
-from oracle import MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle  # noqa: E402
+from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle  # noqa: E402
 from synth import (CONFIGS, asr_logprobs, generate_model, make_config_model, phrase_states,  # noqa: E402
                    seed_for, tiny_model, uniform_states)
 
@@ -426,6 +426,48 @@ def test_fused_topk_odd_vocab_and_bad_state(dev):
     ot, osc, onx = o.fused_topk(asr[good], 1.1, 7, states[good])
     assert np.array_equal(t[good], ot) and np.array_equal(n[good], onx)
     assert np.abs(s_[good] - osc).max() <= TOL
+
+
+def aed_pair():
+    return pair("aed", lambda: generate_model(1024, [1024, 20000, 30000, 20000], 1.05, seed=77, bos_eos=True))
+
+
+def test_aed_advance_and_final_weights(dev):
+    m, lm, o = aed_pair()
+    assert lm.start_state == o.start_state
+    states = np.concatenate([[lm.start_state, 0], uniform_states(m, 3000, seed=78)]).astype(np.int32)
+    check_advance("aed model", m, lm, o, states, dev)
+    case("final weights")
+    fin = lm.final_weights(torch.from_numpy(states).to(dev))
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    assert np.array_equal(fin.cpu().numpy(), o.final(states))
+
+
+def test_aed_greedy_step_and_decode(dev):
+    m, lm, o = aed_pair()
+    V = m.vocab_size
+    B, T = 48, 60
+    asr = asr_logprobs((B, T, V + 1), seed=79, blank_boost=1.5)     # class V is <eos>
+    starts = np.full(B, lm.start_state, np.int32)
+    starts[B // 2:] = uniform_states(m, B - B // 2, seed=80)
+    for lam in (0.0, 0.6, 2.0):
+        check_decode(f"aed per-frame lambda={lam}", lm, o, asr, MODE_AED, lam, starts, dev)
+        case(f"aed decode launch lambda={lam}")
+        gl, gs, fin, _ = gpu_decode_launch(lm, asr, MODE_AED, lam, starts, dev)
+        ol, os_ = o.decode(asr, MODE_AED, lam, starts, nthreads=NTHREADS)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+        print(f"  aed lambda={lam}: <eos> labels {(gl == V).mean():.3f}", flush=True)
+
+
+def test_aed_mode_needs_final_weights(dev):
+    m, lm, o = cfg_pair(1)
+    asr = torch.zeros((2, m.vocab_size + 1), device=dev)
+    st = torch.zeros(2, dtype=torch.int32, device=dev)
+    with pytest.raises(ng.NgpuError):
+        lm.fused_greedy_step(asr, 0.5, st, mode=ng.NGPU_FUSION_AED)
+    with pytest.raises(ng.NgpuError):
+        lm.final_weights(st)
 
 
 def test_fused_out_of_range_state(dev):

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(lib):
     assert sorted(ng.EXPORTED) == decl
 
 
-HDR_FMT = "<IiiiqqQQQQQQQQ11i4x10Q"
+HDR_FMT = "<IiiiqqQQQQQQQQ11i4x10QQii"
 
 
 def parse_image(img):
@@ -51,12 +51,14 @@ def parse_image(img):
     o_st, o_ch, o_dw, o_dt, o_tok, o_w, o_to, total = f[6:14]
     first = list(f[14:25])
     off_order = list(f[25:35])
+    off_final, start_state, has_final = f[35:38]
     assert magic == 0x324D4C4E and total == len(img)
     return dict(V=V, N=N, R=R, S=S, A=A3, first=first, off_order=off_order, raw=raw, o_ch=o_ch,
                 dense_w=np.frombuffer(raw, np.float32, R * V, o_dw).reshape(R, V),
                 dense_to=np.frombuffer(raw, np.int32, R * V, o_dt).reshape(R, V),
                 tok=np.frombuffer(raw, np.int32, A3, o_tok), w=np.frombuffer(raw, np.float32, A3, o_w),
-                to=np.frombuffer(raw, np.int32, A3, o_to))
+                to=np.frombuffer(raw, np.int32, A3, o_to), start_state=start_state,
+                final=np.frombuffer(raw, np.float32, S, off_final) if has_final else None)
 
 
 def chain_of(im, s):
@@ -118,6 +120,53 @@ def test_image_walk_matches_oracle(which):
         sc, n = walk_image(im, int(s))
         assert np.array_equal(n, nx[i]), (which, s)
         assert np.array_equal(sc, s32[i]), (which, s)   # same fp32 fold: bit-exact
+
+
+def test_bos_eos_image_matches_oracle():
+    """<s>/</s> models: numbering, rows, start state and final weights vs the oracle."""
+    for seed in (3, 7):
+        m = generate_model(24, [24, 180, 240, 200], 1.0, seed=seed, bos_eos=True)
+        lm = ng.NgpuLM.from_model(m, shuffle_seed=seed)
+        o = Oracle.from_model(m)
+        assert lm.num_states == o.num_states == m.num_states
+        assert lm.start_state == o.start_state == m.start_state
+        assert lm.state_context(lm.start_state) == (24,)
+        im = parse_image(lm.host_image())
+        states = np.arange(m.num_states, dtype=np.int32)
+        s32, nx, _ = o.advance(states)
+        for s_ in states:
+            sc, n = walk_image(im, int(s_))
+            assert np.array_equal(n, nx[s_]) and np.array_equal(sc, s32[s_])
+        assert np.array_equal(im["final"], o.final(states))      # same fp32 fold: bit-exact
+
+
+def test_bos_eos_build_errors():
+    V = 3
+    order = np.array([1, 1, 1, 1, 1, 2, 2], np.int32)
+    tokens = np.array([[0, -1], [1, -1], [2, -1], [3, -1], [4, -1], [3, 0], [0, 4]], np.int32)
+    W = np.array([-1, -1, -1, -99, -2, -0.5, -0.5], np.float32)
+    B = np.zeros(7, np.float32)
+    lib = ng.load_library()
+
+    def build(o, t, w, b, flags):
+        o, t, w, b = (np.ascontiguousarray(x) for x in (o, t, w, b))
+        lst = ng._NgramList(len(o), 2, o.ctypes.data, t.ctypes.data, w.ctypes.data, b.ctypes.data)
+        h = ctypes.c_void_p()
+        rc = lib.ngpu_lm_build(ctypes.byref(lst), V, float("nan"), flags, ctypes.byref(h))
+        if rc == 0:
+            lib.ngpu_lm_free(h)
+        return rc
+    assert build(order, tokens, W, B, 1) == 0
+    assert build(order, tokens, W, B, 0) == -2                 # ids V, V+1 without the flag
+    bad = tokens.copy(); bad[6] = [4, 0]                       # </s> opening an n-gram
+    assert build(order, bad, W, B, 1) == -2
+    bad = tokens.copy(); bad[5] = [0, 3]                       # <s> closing an n-gram
+    assert build(order, bad, W, B, 1) == -2
+    keep = np.array([1, 1, 1, 0, 1, 0, 1], bool)               # no <s> unigram
+    assert build(order[keep], tokens[keep], W[keep], B[keep], 1) == -7
+    keep = np.array([1, 1, 1, 1, 0, 1, 0], bool)               # no </s> unigram, no <unk>
+    assert build(order[keep], tokens[keep], W[keep], B[keep], 1) == -7
+    assert build(order, tokens, W, B, 4) == -1                 # unknown flag
 
 
 def test_numbering_matches_oracle_on_shuffled_lists():
@@ -202,7 +251,7 @@ def test_build_error_codes():
     Wn = W.copy(); Wn[2] = np.nan
     assert _raw_build(3, 3, o, t, Wn, B)[0] == -10
     assert _raw_build(ng.MAX_VOCAB + 1, 3, o, t, W, B)[0] == -11
-    assert _raw_build(3, 3, o, t, W, B, flags=1)[0] == -1
+    assert _raw_build(3, 3, o, t, W, B, flags=2)[0] == -1
 
 
 def test_queries_before_upload_fail_cleanly():

@@ -19,7 +19,7 @@ import numpy as np
 import pytest
 
 import oracle
-from oracle import MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle
+from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle
 from oracle.bruteforce import BruteForce
 from synth import (asr_logprobs, generate_model, make_config_model, state_ids_of, tiny_model,
                    uniform_states)
@@ -358,6 +358,74 @@ def test_topk_reductions(oracle_lib):
         # the fused score is lambda * lm + asr with one rounding
         assert np.abs(sc[b] - (np.float64(np.float32(1.3)) * s32[0] + asr[b])[tok[b]]).max() < 1e-5
         assert (nx[b] == n[0][tok[b]]).all()
+
+
+def bos_eos_model(seed=3, V=20, counts=(20, 150, 200, 150)):
+    return generate_model(V, list(counts), 1.0, seed=seed, bos_eos=True)
+
+
+def test_bos_eos_normalisation_includes_final_weight(oracle_lib):
+    """With </s> every context sums to one over the V tokens and </s>, so the
+    final weight is pinned by the same invariant as the scores."""
+    for seed in (3, 4):
+        m = bos_eos_model(seed)
+        o = Oracle.from_model(m)
+        S = o.num_states
+        states = np.arange(S, dtype=np.int32)
+        s32, nx, s64 = o.advance(states, want64=True)
+        fin = o.final(states).astype(np.float64)
+        tot = np.exp(s64).sum(axis=1) + np.exp(fin)
+        assert np.abs(tot - 1).max() < 1e-5
+        assert o.start_state == m.start_state and o.state_context(o.start_state) == (m.vocab_size,)
+
+
+def test_bos_eos_bruteforce_histories(oracle_lib):
+    """Sentences start in <s>: every history after <s> reaches the longest listed
+    context, and its token and </s> scores follow the recursion."""
+    m = bos_eos_model(5, V=5, counts=(5, 18, 20, 16))
+    o = Oracle.from_model(m)
+    bf = BruteForce.from_model(m)
+    V, eos = m.vocab_size, m.vocab_size + 1
+    S = o.num_states
+    s32, nx, s64 = o.advance(np.arange(S, dtype=np.int32), want64=True)
+    fin = o.final(np.arange(S, dtype=np.int32))
+    for L in range(0, 4):
+        for w in itertools.product(range(V), repeat=L):
+            h = (V,) + w
+            st = o.start_state
+            for t in w:
+                st = int(nx[st, t])
+            assert o.state_context(st) == bf.state_context(h)
+            for v in range(V):
+                assert abs(s64[st, v] - bf.score(h, v)) < 1e-9
+            assert abs(fin[st] - bf.score(h, eos)) < 1e-5
+
+
+def test_aed_mode_rules(oracle_lib):
+    """lambda = 0: the raw argmax over V tokens and <eos> (class V); <eos> keeps
+    the state; otherwise the state follows the token."""
+    m = bos_eos_model(6)
+    o = Oracle.from_model(m)
+    V = m.vocab_size
+    rng = np.random.default_rng(17)
+    states = rng.integers(0, o.num_states, 60).astype(np.int32)
+    asr = asr_logprobs((60, V + 1), seed=18)
+    asr[:10, V] = 1.0                            # <eos> wins for ten rows
+    st = states.copy()
+    tok = o.greedy_step(asr, MODE_AED, 0.0, st)
+    assert tok.tolist() == np.argmax(asr, axis=1).tolist()
+    _, nx, _ = o.advance(states)
+    for b in range(60):
+        exp = states[b] if tok[b] == V else nx[b, tok[b]]
+        assert st[b] == exp
+    # lambda > 0: <eos> is scored with the final weight
+    st = states.copy()
+    tok = o.greedy_step(asr, MODE_AED, 0.8, st)
+    s32, _, _ = o.advance(states)
+    fin = o.final(states)
+    for b in range(60):
+        f = np.append(np.float32(0.8) * s32[b] + asr[b, :V], np.float32(0.8) * fin[b] + asr[b, V])
+        assert tok[b] == int(np.argmax(f)) or abs(f.max() - f[tok[b]]) < 1e-6
 
 
 def test_generator_and_oracle_number_states_alike(oracle_lib):

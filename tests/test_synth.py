@@ -3,7 +3,7 @@
 import numpy as np
 
 from synth import (CONFIGS, asr_logprobs, generate_model, lookup_ids, make_config_model,
-                   phrase_states, tiny_model, uniform_states)
+                   phrase_states, state_ids_of, tiny_model, uniform_states)
 
 
 def _closure_ok(model):
@@ -55,6 +55,24 @@ def test_tiny_models_closed_and_normalised():
     m = tiny_model(9, 3, seed=21, n_unigrams=6)
     _closure_ok(m)
     _construction_identity(m)
+
+
+def test_bos_eos_models_closed_and_normalised():
+    for seed in range(3):
+        m = generate_model(16, [16, 120, 150, 100], 1.0, seed=seed, bos_eos=True)
+        V = m.vocab_size
+        o, t, W, B = m.to_list()
+        for i in range(len(o)):
+            row = t[i, :o[i]].tolist()
+            assert V not in row[1:] and (V + 1) not in row[:-1]
+        # every context sums to one over the V tokens and </s> (construction identity)
+        z1 = np.exp(m.levels[1].W.astype(np.float64))[m.levels[1].tok != V].sum()
+        assert abs(z1 - 1) < 1e-6
+        for k in range(2, m.max_order + 1):
+            lv = m.levels[k]
+            assert (m.levels[k - 1].tok[lv.pid] != V + 1).all()     # </s> is never extended
+            assert (lv.tok != V).all()                             # <s> is never predicted
+        assert m.start_state == state_ids_of(m, np.array([[V]]))[0]
 
 
 def test_deterministic_from_seed():

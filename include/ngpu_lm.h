@@ -236,6 +236,28 @@ int ngpu_lm_query_bytes(const ngpu_lm *lm, const int32_t *h_states, int64_t B,
  * library build; it is exposed for saving an image and for white-box tests. */
 int ngpu_lm_host_image(const ngpu_lm *lm, const void **data, size_t *bytes);
 
+/* ARPA text (Section 2.1: "W context token B" lines, base-10 logarithms, as
+ * KenLM writes them) parsed into an n-gram list for ngpu_lm_build.
+ * vocab[0..V-1]: the scored vocabulary as words (NUL-terminated, distinct,
+ * without <unk>, <s>, </s>); every other word of the file is an error
+ * (NGPU_E_TOKEN_RANGE).  Weights become natural logarithms: x * ln 10 in
+ * double, rounded once to fp32.  The <unk> unigram's weight is returned as
+ * the <unk> weight; longer n-grams containing <unk> are dropped.  With
+ * NGPU_BUILD_BOS_EOS, <s> and </s> become tokens V and V + 1; without it,
+ * n-grams containing them are dropped (a closed file stays closed either
+ * way).  The header's n-gram counts must match the file.  text need not be
+ * NUL-terminated; it is read only during the call.  On success *out owns the
+ * list (free with ngpu_arpa_free). */
+typedef struct ngpu_arpa ngpu_arpa;
+int ngpu_arpa_parse(const char *text, size_t len, const char *const *vocab, int32_t V, uint32_t flags,
+                    ngpu_arpa **out);
+
+/* The parsed list (arrays owned by a, valid until ngpu_arpa_free) and the
+ * <unk> weight (NaN when the file has no <unk> unigram). */
+int ngpu_arpa_list(const ngpu_arpa *a, ngpu_ngram_list *list, float *unk_logprob);
+
+void ngpu_arpa_free(ngpu_arpa *a);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char *ngpu_lm_last_error(void);
 

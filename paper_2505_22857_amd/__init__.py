@@ -35,6 +35,7 @@ EXPORTED = [
     "ngpu_lm_fused_topk", "ngpu_lm_start_state", "ngpu_lm_final_weights",
     "ngpu_lm_check_states",
     "ngpu_lm_query_bytes", "ngpu_lm_host_image", "ngpu_lm_last_error",
+    "ngpu_arpa_parse", "ngpu_arpa_list", "ngpu_arpa_free",
 ]
 
 
@@ -88,10 +89,15 @@ def load_library(path: str = LIB_PATH):
     lib.ngpu_lm_check_states.argtypes = [vp, vp, ctypes.POINTER(i64)]
     lib.ngpu_lm_query_bytes.argtypes = [vp, vp, i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ngpu_lm_host_image.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(ctypes.c_size_t)]
+    lib.ngpu_arpa_parse.argtypes = [ctypes.c_char_p, ctypes.c_size_t, vp, i32, ctypes.c_uint32,
+                                    ctypes.POINTER(vp)]
+    lib.ngpu_arpa_list.argtypes = [vp, ctypes.POINTER(_NgramList), ctypes.POINTER(ctypes.c_float)]
+    lib.ngpu_arpa_free.argtypes = [vp]
+    lib.ngpu_arpa_free.restype = None
     lib.ngpu_lm_last_error.argtypes = []
     lib.ngpu_lm_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
-        if name not in ("ngpu_lm_free", "ngpu_lm_device_bytes", "ngpu_lm_last_error"):
+        if name not in ("ngpu_lm_free", "ngpu_lm_device_bytes", "ngpu_lm_last_error", "ngpu_arpa_free"):
             getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -116,6 +122,37 @@ def _dptr(t, dtype, name):
     if t.dtype != dtype or not t.is_contiguous():
         raise TypeError(f"{name} must be a contiguous {dtype} tensor")
     return ctypes.c_void_p(t.data_ptr())
+
+
+def parse_arpa(text, vocab, bos_eos: bool = False):
+    """Parse ARPA text with the library's reader.
+
+    Returns ``(max_order, order, tokens, logprob, backoff, unk_logprob)`` as
+    numpy copies (natural-log fp32 weights), ready for ``NgpuLM``."""
+    lib = load_library()
+    data = text.encode() if isinstance(text, str) else bytes(text)
+    words = [w.encode() for w in vocab]
+    arr = (ctypes.c_char_p * len(words))(*words)
+    h = ctypes.c_void_p()
+    _check(lib.ngpu_arpa_parse(data, len(data), ctypes.cast(arr, ctypes.c_void_p), len(words),
+                               NGPU_BUILD_BOS_EOS if bos_eos else 0, ctypes.byref(h)))
+    try:
+        lst = _NgramList()
+        unk = ctypes.c_float()
+        _check(lib.ngpu_arpa_list(h, ctypes.byref(lst), ctypes.byref(unk)))
+        M, N = int(lst.num_ngrams), int(lst.max_order)
+
+        def arr_of(ptr, ct, n):
+            if n == 0:
+                return np.zeros(0, np.dtype(ct))
+            return np.ctypeslib.as_array(ctypes.cast(ptr, ctypes.POINTER(ct)), shape=(n,)).copy()
+        order = arr_of(lst.order, ctypes.c_int32, M)
+        tokens = arr_of(lst.tokens, ctypes.c_int32, M * N).reshape(M, N)
+        logprob = arr_of(lst.logprob, ctypes.c_float, M)
+        backoff = arr_of(lst.backoff, ctypes.c_float, M)
+        return N, order, tokens, logprob, backoff, float(unk.value)
+    finally:
+        lib.ngpu_arpa_free(h)
 
 
 class NgpuLM:
@@ -292,5 +329,5 @@ class NgpuLM:
         return int(hbm.value), int(tot.value)
 
 
-__all__ = ["NgpuLM", "NgpuError", "load_library", "LIB_PATH", "EXPORTED", "NGPU_BUILD_BOS_EOS",
+__all__ = ["NgpuLM", "NgpuError", "load_library", "parse_arpa", "LIB_PATH", "EXPORTED", "NGPU_BUILD_BOS_EOS",
            "NGPU_FUSION_PLAIN", "NGPU_FUSION_CTC", "NGPU_FUSION_TRANSDUCER", "NGPU_FUSION_AED"]

@@ -9,7 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB_PATH = os.path.join(HERE, "libngpu_lm.so")
-SOURCES = ["api.cpp", "trie_build.cpp", "advance.hip", "fused_step.hip"]
+SOURCES = ["api.cpp", "trie_build.cpp", "arpa.cpp", "advance.hip", "fused_step.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -73,6 +73,11 @@ ngpu::DevTrie dev_view(const ngpu_lm *lm) {
 
 }  // namespace
 
+int ngpu::set_error(int code, const std::string &msg) {
+    g_last_error = msg;
+    return code;
+}
+
 extern "C" {
 
 const char *ngpu_lm_last_error(void) { return g_last_error.c_str(); }

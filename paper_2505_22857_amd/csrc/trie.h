@@ -115,6 +115,8 @@ struct ngpu_lm {
 };
 
 namespace ngpu {
+// api.cpp: records the thread's last error message and returns code
+int set_error(int code, const std::string &msg);
 // trie_build.cpp
 int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags, ngpu_lm *lm, std::string *err);
 }  // namespace ngpu

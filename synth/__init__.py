@@ -15,9 +15,11 @@ from .ngram import NgramModel, generate_model, lookup_ids, state_ids_of
 from .configs import CONFIGS, ConfigSpec, make_config_model, seed_for
 from .workloads import (asr_logprobs, uniform_states, phrase_states,
                         tiny_model)
+from .arpa import write_arpa, bpe_like_vocab
 
 __all__ = [
     "NgramModel", "generate_model", "lookup_ids", "state_ids_of",
     "CONFIGS", "ConfigSpec", "make_config_model", "seed_for",
     "asr_logprobs", "uniform_states", "phrase_states", "tiny_model",
+    "write_arpa", "bpe_like_vocab",
 ]

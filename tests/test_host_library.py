@@ -29,7 +29,7 @@ def lib():
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(ngpu_lm_\w+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(ngpu_(?:lm|arpa)_\w+)\s*\(", src)))
 
 
 def test_library_exports_every_declared_symbol(lib):

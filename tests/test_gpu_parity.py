@@ -470,6 +470,63 @@ def test_aed_mode_needs_final_weights(dev):
         lm.final_weights(st)
 
 
+def test_graph_capture_replays_match_eager(dev):
+    """The per-frame steps and an advance captured in one HIP graph (the paper
+    runs its decoding steps in CUDA graphs) give the eager results on every
+    replay, with eager work in between."""
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    B, T = 32, 12
+    asr_np = asr_logprobs((T, B, V + 1), seed=91, blank_boost=2.0)
+    starts = uniform_states(m, B, seed=92)
+    asr = torch.from_numpy(asr_np).to(dev)
+    st = torch.from_numpy(starts).to(dev)
+    prev = torch.full((B,), V, dtype=torch.int32, device=dev)
+    toks = torch.empty((T, B), dtype=torch.int32, device=dev)
+    sc = torch.empty((B, V), dtype=torch.float32, device=dev)
+    nx = torch.empty((B, V), dtype=torch.int32, device=dev)
+    st0 = st.clone()
+
+    def body():
+        for t in range(T):
+            lm.fused_greedy_step(asr[t], 0.5, st, prev, mode=ng.NGPU_FUSION_CTC, tokens=toks[t])
+        lm.advance(st, sc, nx)
+
+    # eager reference
+    body()
+    torch.cuda.synchronize()
+    ref = [x.clone() for x in (toks, st, prev, sc, nx)]
+    case("graph capture of 12 fused steps and one advance")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):                 # warm the libraries on the capture stream
+        st.copy_(st0)
+        prev.fill_(V)
+        body()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    st.copy_(st0)
+    prev.fill_(V)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        body()
+    for r in range(4):
+        st.copy_(st0)
+        prev.fill_(V)
+        toks.fill_(-9)
+        sc.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip((toks, st, prev, sc, nx), ref):
+            assert torch.equal(a, b), f"replay {r} differs"
+        _ = lm.advance(st)                        # eager work between replays
+        torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    ol, os_ = o.decode(np.ascontiguousarray(asr_np.transpose(1, 0, 2)), MODE_CTC, 0.5, starts)
+    assert np.array_equal(ref[0].cpu().numpy().T, ol)
+
+
 def test_fused_out_of_range_state(dev):
     m, lm, o = cfg_pair(1)
     V = m.vocab_size

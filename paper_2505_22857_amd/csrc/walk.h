@@ -149,15 +149,19 @@ __device__ __forceinline__ void store_stripe(const ArcStripe &st, float acc, flo
     }
 }
 
-// The walk of uniform state s into (ls, ln).  When pf_src is given, pf_n words
-// from it are also copied into pf_dst once the record is in (a prefetch that
-// rides along with the dense row and the arcs).
-__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane,
-                                                   const float *pf_src = nullptr, float *pf_dst = nullptr,
-                                                   int pf_n = 0) {
-    int nlev;
+// Issues the load of state s's chain record (s uniform and valid); nlev is its
+// number of levels.  The record is consumed by walk_record().
+__device__ __forceinline__ int4 fetch_record(const DevTrie &t, int s, int lane, int &nlev) {
     const unsigned char *rp = chain_record(t, s, nlev);
-    const int4 rec = load_record(rp, nlev, lane);
+    return load_record(rp, nlev, lane);
+}
+
+// The walk of a fetched record into (ls, ln).  When pf_src is given, pf_n
+// words from it are also copied into pf_dst once the record is in (a prefetch
+// that rides along with the dense row and the arcs).
+__device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
+                                                 int lane, const float *pf_src = nullptr, float *pf_dst = nullptr,
+                                                 int pf_n = 0) {
     const ChainHead h = head_of(rec);
     dense_to_lds(t, h.dense_row, ls, ln, lane);
     if (pf_src) copy_to_lds_dword(pf_src, pf_dst, pf_n, lane);
@@ -179,6 +183,13 @@ __device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, floa
     return h;
 }
 
+// The walk of uniform state s into (ls, ln).
+__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
+    int nlev;
+    const int4 rec = fetch_record(t, s, lane, nlev);
+    return walk_record(t, rec, nlev, ls, ln, lane);
+}
+
 // Final (score, next state) of one LDS slot.
 __device__ __forceinline__ void slot_value(const ChainHead &h, float x, int n, float &score, int &next) {
     if (n & kFinal) {
@@ -190,16 +201,32 @@ __device__ __forceinline__ void slot_value(const ChainHead &h, float x, int n, f
     }
 }
 
-// Wave-wide maximum of a 64-bit key.
+// One step of the wave maximum: each lane takes the larger of its key and the
+// key DPP control CTRL moves into it (lanes with no source, or outside
+// ROW_MASK, see 0, which never wins since keys are unsigned).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ unsigned long long max_step(unsigned long long k) {
+    const int lo = int(unsigned(k & 0xffffffffu));
+    const int hi = int(unsigned(k >> 32));
+    const unsigned olo = unsigned(__builtin_amdgcn_update_dpp(0, lo, CTRL, ROW_MASK, 0xf, true));
+    const unsigned ohi = unsigned(__builtin_amdgcn_update_dpp(0, hi, CTRL, ROW_MASK, 0xf, true));
+    const unsigned long long o = (static_cast<unsigned long long>(ohi) << 32) | olo;
+    return o > k ? o : k;
+}
+
+// Wave-wide maximum of a 64-bit key, uniform in every lane.  An inclusive scan
+// within each row of 16 lanes (row_shr 1, 2, 4, 8), then row 15 broadcast into
+// rows 1 and 3 and row 31 into rows 2 and 3, leaves the maximum in lane 63.
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long k) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        unsigned lo = __shfl_xor((unsigned)(k & 0xffffffffu), off, kWave);
-        unsigned hi = __shfl_xor((unsigned)(k >> 32), off, kWave);
-        unsigned long long o = ((unsigned long long)hi << 32) | lo;
-        k = o > k ? o : k;
-    }
-    return k;
+    k = max_step<0x111, 0xf>(k);
+    k = max_step<0x112, 0xf>(k);
+    k = max_step<0x114, 0xf>(k);
+    k = max_step<0x118, 0xf>(k);
+    k = max_step<0x142, 0xa>(k);
+    k = max_step<0x143, 0xc>(k);
+    const unsigned lo = unsigned(__builtin_amdgcn_readlane(int(unsigned(k & 0xffffffffu)), kWave - 1));
+    const unsigned hi = unsigned(__builtin_amdgcn_readlane(int(unsigned(k >> 32)), kWave - 1));
+    return (static_cast<unsigned long long>(hi) << 32) | lo;
 }
 
 // Argmax key: larger value first, then smaller index.  -0 counts as +0 so
@@ -214,5 +241,35 @@ __device__ __forceinline__ unsigned long long argmax_key(float x, int idx) {
 __device__ __forceinline__ int argmax_index(unsigned long long key) {
     return (int)(0xffffffffu - (unsigned)(key & 0xffffffffu));
 }
+
+// The value an argmax key was made from (-0 comes back as +0).
+__device__ __forceinline__ float key_value(unsigned long long key) {
+    unsigned u = unsigned(key >> 32);
+    u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
+    return __uint_as_float(u);
+}
+
+// Per-lane running argmax over indices taken in ascending order: a strictly
+// larger value replaces the best, so the lane keeps its lowest index among
+// equal values.  kNone marks a lane that has seen nothing above -inf.
+constexpr int kNone = 0x7fffffff;
+
+__device__ __forceinline__ void take_max(float f, int v, float &bx, int &bi) {
+    if (f > bx) {
+        bx = f;
+        bi = v;
+    }
+}
+
+// Wave argmax of the lanes' (bx, bi): the lowest index among the largest
+// values, and that value.  kNone when every value was -inf.
+__device__ __forceinline__ int wave_argmax(float bx, int bi, float &best) {
+    const unsigned long long k = wave_max_u64(argmax_key(bx, bi));
+    best = key_value(k);
+    return argmax_index(k);
+}
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 }  // namespace ngpu

@@ -371,6 +371,89 @@ def test_fused_ties_lambda_zero_and_all_blank(dev):
     assert (gl == V).all() and (gs == starts[:3, None]).all()
 
 
+def _edge_frames(V, B):
+    """Frames whose argmax hinges on -inf and on ties across lanes and stripes
+    (tokens go four to a lane in stripes of 256)."""
+    ninf = -np.inf
+    asr = asr_logprobs((B, 8, V + 1), seed=13, blank_boost=0.5)
+    asr[:, 0, :] = ninf                                    # every class at -inf
+    asr[:, 1, :V] = ninf                                   # tokens at -inf, blank finite
+    asr[:, 1, V] = -1.0
+    for t, (i, j) in zip((2, 3, 4), ((252, 256), (5, 261), (767, 1023))):
+        asr[:, t, :] = -9.0                                # two-way ties at the top:
+        asr[:, t, i] = asr[:, t, j] = 5.0                  # lane 63 vs lane 0, same lane, same lane
+    asr[:, 5, :] = ninf                                    # one finite token, blank -inf in half the rows
+    asr[:, 5, 600] = -1.0
+    asr[B // 2:, 5, V] = -2.0
+    asr[:, 6, :] = -4.0                                    # -0 and +0 tie at the top
+    asr[:, 6, 10] = -0.0
+    asr[:, 6, 3] = 0.0
+    return asr
+
+
+@pytest.mark.parametrize("mode", [MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER])
+def test_fused_minus_inf_and_lane_ties(dev, mode):
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    B = 40
+    asr = _edge_frames(V, B)
+    if mode == MODE_PLAIN:
+        asr = np.ascontiguousarray(asr[:, :, :V])
+    starts = uniform_states(m, B, seed=14)
+    for lam in (0.0, 0.5, -1.0):
+        check_decode(f"edge frames mode={mode} lambda={lam}", lm, o, asr, mode, lam, starts, dev)
+        case(f"edge frames decode launch mode={mode} lambda={lam}")
+        gl, gs, _, _ = gpu_decode_launch(lm, asr, mode, lam, starts, dev)
+        ol, os_ = o.decode(asr, mode, lam, starts, nthreads=NTHREADS)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+    if mode == MODE_PLAIN:
+        assert (gl[:, 0] == 0).all()                       # all -inf: the first token
+    else:
+        assert (gl[:, 0] == 0).all() and (gl[:, 1] == V).all()
+
+
+def test_aed_minus_inf_frames(dev):
+    m, lm, o = aed_pair()
+    V = m.vocab_size
+    B = 24
+    asr = _edge_frames(V, B)
+    starts = uniform_states(m, B, seed=15)
+    for lam in (0.0, 0.7):
+        check_decode(f"aed edge frames lambda={lam}", lm, o, asr, MODE_AED, lam, starts, dev)
+        gl, gs, _, _ = gpu_decode_launch(lm, asr, MODE_AED, lam, starts, dev)
+        ol, os_ = o.decode(asr, MODE_AED, lam, starts, nthreads=NTHREADS)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+        assert (gl[:, 0] == 0).all() and (gl[:, 1] == V).all()
+
+
+def test_max_vocabulary(dev):
+    """V = 8192, the largest vocabulary the library takes: the LDS rows of
+    every kernel at their largest."""
+    m, lm, o = pair("V8192", lambda: generate_model(8192, [8192, 40000, 30000], 1.0, seed=8192))
+    V = m.vocab_size
+    assert V == 8192
+    states = uniform_states(m, 700, seed=16)
+    check_advance("V=8192", m, lm, o, states, dev)
+    B, T = 20, 12
+    asr = asr_logprobs((B, T, V + 1), seed=17, blank_boost=1.0)
+    starts = states[:B]
+    for mode in (MODE_PLAIN, MODE_CTC):
+        a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+        check_decode(f"V=8192 mode={mode}", lm, o, a, mode, 0.5, starts, dev)
+        case(f"V=8192 decode launch mode={mode}")
+        gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+    case("V=8192 top-k k=20")
+    a0 = np.ascontiguousarray(asr[:, 0, :V])
+    tok, sc, nx = lm.fused_topk(torch.from_numpy(a0).to(dev), 0.5, 20, torch.from_numpy(starts).to(dev))
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    ot, osc, onx = o.fused_topk(a0, 0.5, 20, starts)
+    assert np.array_equal(tok.cpu().numpy(), ot) and np.array_equal(nx.cpu().numpy(), onx)
+    assert np.abs(sc.cpu().numpy() - osc).max() <= TOL
+
+
 def test_fused_strided_asr_rows(dev):
     """asr rows with a leading dimension larger than V + 1."""
     m, lm, o = cfg_pair(1)

@@ -13,8 +13,11 @@ second over the timed steps.  The same run also reports:
   ``traffic`` is the measured HBM bytes per launch from the committed rocprofv3
   counter summary when it was taken on the current kernel source, else null;
 * latency of a single 512-hypothesis call (median of 100);
+* the same work as 128 separate 512-hypothesis calls on 8 streams, captured in
+  one HIP graph;
 * the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame,
   and the same decode of 1000 frames as one launch;
+* plain fusion on the 200k-n-gram 4-gram at B = 32 hypotheses x 200 steps;
 * cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
   host cores.
 """
@@ -77,6 +80,7 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 512 MiB device copy and fill (counter calibration)")
     ap.add_argument("--advance-only", action="store_true", help="skip the fused step and the oracle")
+    ap.add_argument("--no-graph", action="store_true", help="skip the graph of 512-hypothesis calls")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
@@ -172,6 +176,46 @@ def main():
         f"(min {kern_ms.min():.3f}), {achieved:.0f} GB/s algorithmic HBM, "
         f"{total_bytes / (mean_ms * 1e-3) / 1e9:.0f} GB/s incl. cache-resident rows")
 
+    # ---- the same work as R separate 512-hypothesis calls in one HIP graph over 8 streams
+    graph = None
+    if not args.no_graph:
+        streams = [torch.cuda.Stream() for _ in range(8)]
+
+        def fan_out():
+            main_s = torch.cuda.current_stream()
+            for i, st_ in enumerate(streams):
+                st_.wait_stream(main_s)
+                with torch.cuda.stream(st_):
+                    for r in range(i, R, len(streams)):
+                        sl = slice(r * Bb, (r + 1) * Bb)
+                        lm.advance(states[sl], scores[sl], nxt[sl])
+            for st_ in streams:
+                main_s.wait_stream(st_)
+
+        fan_out()                                   # eager once on the same streams
+        torch.cuda.synchronize()
+        g_adv = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_adv):
+            fan_out()
+        for _ in range(3):
+            g_adv.replay()
+        torch.cuda.synchronize()
+        reps = 20
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(reps):
+            g_adv.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        assert lm.check_states() == 0
+        g_ms = g0.elapsed_time(g1) / reps
+        graph = {"workload": f"{R} calls of B={Bb} on 8 streams, one HIP graph replay",
+                 "ms": g_ms, "scores_per_s": B * V / (g_ms * 1e-3),
+                 "algorithmic_gbps": hbm_bytes / (g_ms * 1e-3) / 1e9}
+        log(f"advance as {R} graph-captured B={Bb} calls on 8 streams: {g_ms:.3f} ms per replay, "
+            f"{graph['scores_per_s']:.3g} scores/s")
+        del g_adv
+
     if args.advance_only:
         return
 
@@ -232,6 +276,47 @@ def main():
         f"{fused_decode['frames_per_s']:.3g} frames/s")
     del asr, asr_bt
 
+    # ---- plain fusion on the 200k 4-gram (config 2 shape): B = 32 hypotheses x 200 steps
+    pspec = CONFIGS[2]
+    pmodel = make_config_model(2)
+    plm = ng.NgpuLM.from_model(pmodel).upload(dev)
+    Bp, Tp = pspec.batch, pspec.steps
+    gp = torch.Generator(device=dev)
+    gp.manual_seed(seed_for(2))
+    pasr = torch.log_softmax(torch.randn((Tp, Bp, V), generator=gp, device=dev) * 3.0, dim=-1)
+    pstart = torch.from_numpy(uniform_states(pmodel, Bp, seed=seed_for(2) + 77)).to(dev)
+    pst = pstart.clone()
+    ptok = torch.empty(Bp, dtype=torch.int32, device=dev)
+    for t in range(20):
+        plm.fused_greedy_step(pasr[t], pspec.lam, pst, tokens=ptok)
+    pst.copy_(pstart)
+    torch.cuda.synchronize()
+    f0.record(stream)
+    for t in range(Tp):
+        plm.fused_greedy_step(pasr[t], pspec.lam, pst, tokens=ptok)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    p_ms = f0.elapsed_time(f1)
+    plabels = torch.empty((Bp, Tp), dtype=torch.int32, device=dev)
+    pasr_bt = pasr.permute(1, 0, 2)
+    pd = []
+    for _ in range(4):
+        pst.copy_(pstart)
+        f0.record(stream)
+        plm.fused_greedy_decode(pasr_bt, pspec.lam, pst, labels=plabels)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        pd.append(f0.elapsed_time(f1))
+    assert plm.check_states() == 0
+    pdm = float(np.median(pd[1:]))
+    fused_plain = {"workload": f"plain fusion, 4-gram V={V} 200k n-grams, B={Bp} hypotheses x {Tp} steps, "
+                               f"lambda={pspec.lam}",
+                   "per_step_launch_us": p_ms * 1e3 / Tp, "one_launch_us_per_step": pdm * 1e3 / Tp,
+                   "steps_per_s_one_launch": Tp / (pdm * 1e-3)}
+    log(f"fused plain (B={Bp}): {fused_plain['per_step_launch_us']:.1f} us/step one launch per step, "
+        f"{fused_plain['one_launch_us_per_step']:.2f} us/step in one decode launch")
+    del plm, pasr, pasr_bt
+
     # ---- CPU oracle on a bounded sample of the same workload
     cpu = None
     if args.cpu_seconds > 0:
@@ -269,6 +354,8 @@ def main():
         "latency_b512_us": lat_us,
         "fused": fused,
         "fused_decode": fused_decode,
+        "fused_plain": fused_plain,
+        "advance_graph_b512": graph,
         "cpu_baseline": cpu,
         "kernel_source_sha256": kernel_source_hash(),
     }

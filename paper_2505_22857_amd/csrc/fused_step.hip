@@ -27,23 +27,25 @@ namespace ngpu {
 
 enum { kPlain = 0, kCtc = 1, kTransducer = 2, kAed = 3 };
 
-// Words of an ASR row buffer in LDS: the V + 1 classes rounded up to whole
-// 256-word stripes, so that the 16-byte reads of the scans stay inside it.
-__host__ __device__ inline int asr_row_words(int V) { return lds_row(V + 1); }
+// Words of an ASR row buffer in LDS: the V tokens rounded up to whole
+// stripes, so that the 16-byte reads of the scans stay inside it.  (Blank or
+// <eos>, class V, travels in a register.)
+__host__ __device__ inline int asr_row_words(int V) { return lds_row(V); }
 
-// Per-lane argmax of row[v] over tokens v < V.  Tokens go in stripes of 256:
-// lane l reads 4 consecutive tokens 4l .. 4l + 3 of each stripe with one
-// 16-byte LDS read, so every lane meets its tokens in ascending order.
-__device__ __forceinline__ void scan_row(const float *row, int V, int lane, float &bx, int &bi) {
-    const int full = V & ~255;
+// Per-lane argmax of row[v] over the owned tokens v < V.  Lane l reads tokens
+// 4l .. 4l + 3 of each owned stripe with one 16-byte LDS read, so every lane
+// meets its tokens in ascending order.
+template <int W>
+__device__ __forceinline__ void scan_row(const float *row, int V, int wave, int lane, float &bx, int &bi) {
+    const int full = V & ~(kStripe - 1);
 #pragma unroll 4
-    for (int c = 0; c < full; c += 256) {
+    for (int c = kStripe * wave; c < full; c += kStripe * W) {
         const int v0 = c + 4 * lane;
         const f32x4 a = *reinterpret_cast<const f32x4 *>(row + v0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) take_max(a[j], v0 + j, bx, bi);
     }
-    if (full < V) {
+    if (full < V && owns_token<W>(full, wave)) {
         const int v0 = full + 4 * lane;
         const f32x4 a = *reinterpret_cast<const f32x4 *>(row + v0);
 #pragma unroll
@@ -52,11 +54,11 @@ __device__ __forceinline__ void scan_row(const float *row, int V, int lane, floa
     }
 }
 
-// Per-lane argmax of fmaf(lambda, lm[v], row[v]) over tokens v < V (v != pv
-// in CTC mode), lm[v] from the walked LDS row; same stripes as scan_row.
-template <int MODE>
+// Per-lane argmax of fmaf(lambda, lm[v], row[v]) over the owned tokens v < V
+// (v != pv in CTC mode), lm[v] from the walked LDS row; same reads as scan_row.
+template <int MODE, int W>
 __device__ __forceinline__ void scan_fused(const ChainHead &h, const float *ls, const int *ln, const float *row,
-                                           float lambda, int pv, int V, int lane, float &bx, int &bi) {
+                                           float lambda, int pv, int V, int wave, int lane, float &bx, int &bi) {
     auto four = [&](int v0, bool tail) {
         const f32x4 x = *reinterpret_cast<const f32x4 *>(ls + v0);
         const i32x4 n = *reinterpret_cast<const i32x4 *>(ln + v0);
@@ -71,21 +73,93 @@ __device__ __forceinline__ void scan_fused(const ChainHead &h, const float *ls, 
             if ((MODE != kCtc || v != pv) && (!tail || v < V)) take_max(f, v, bx, bi);
         }
     };
-    const int full = V & ~255;
+    const int full = V & ~(kStripe - 1);
 #pragma unroll 4
-    for (int c = 0; c < full; c += 256) four(c + 4 * lane, false);
-    if (full < V) four(full + 4 * lane, true);
+    for (int c = kStripe * wave; c < full; c += kStripe * W) four(c + 4 * lane, false);
+    if (full < V && owns_token<W>(full, wave)) four(full + 4 * lane, true);
 }
 
-// One fused greedy step of the wavefront's hypothesis.  row: its V + 1 ASR
-// log-probabilities in LDS (asr_row_words(V) words); they have landed unless
-// ROW_PENDING, in which case their copy was issued just before.  s: valid
-// state (uniform); pv: previous label (CTC).  Returns the label and updates s.
-// All lanes return the same values.
-template <int MODE, bool ROW_PENDING>
-__device__ __forceinline__ int greedy_step(const DevTrie &t, const float *row, float lambda, int &s, int pv,
-                                           float *ls, int *ln, int lane, const float *pf_src = nullptr,
-                                           float *pf_dst = nullptr, int pf_n = 0) {
+// Exchange area of W wavefronts: two alternating buffers of W (key, payload)
+// pairs, so one barrier per exchange suffices (a buffer is written again only
+// after every wavefront has passed the next exchange's barrier).
+struct Exchange {
+    unsigned long long key[2][4];
+    int payload[2][4];
+};
+
+// Waits until this wavefront's LDS writes are done, then for all wavefronts
+// of the workgroup.  The memory clobber keeps the compiler from moving any
+// memory access across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Argmax over the W wavefronts' lanes of (bx, bi): lowest index among the
+// largest values.  Returns the index (kNone when every value was -inf), its
+// value and the payload the winning lane passed in; all uniform.
+template <int W>
+__device__ __forceinline__ int group_argmax(float bx, int bi, int payload, float &best, int &win_payload,
+                                            Exchange *xc, int &xi, int wave, int lane) {
+    const unsigned long long mine = argmax_key(bx, bi);
+    unsigned long long k = wave_max_u64(mine);
+    // the lane whose key won hands over its payload (the lowest such lane: keys are unique but for kNone)
+    const unsigned long long won = __builtin_amdgcn_read_exec() & __ballot(mine == k);
+    const int src = won ? int(__builtin_ctzll(won)) : 0;
+    int pl = __builtin_amdgcn_readlane(payload, src);
+    if (W > 1) {
+        const int buf = xi & 1;
+        ++xi;
+        if (lane == 0) {
+            xc->key[buf][wave] = k;
+            xc->payload[buf][wave] = pl;
+        }
+        lds_barrier();
+#pragma unroll
+        for (int i = 0; i < W; ++i) {
+            const unsigned long long o = xc->key[buf][i];
+            const int op = xc->payload[buf][i];
+            if (o > k) {
+                k = o;
+                pl = op;
+            }
+        }
+        k = (static_cast<unsigned long long>(unsigned(__builtin_amdgcn_readfirstlane(int(unsigned(k >> 32))))) << 32) |
+            unsigned(__builtin_amdgcn_readfirstlane(int(unsigned(k & 0xffffffffu))));
+        pl = __builtin_amdgcn_readfirstlane(pl);
+    }
+    best = key_value(k);
+    win_payload = pl;
+    return argmax_index(k);
+}
+
+// Next state of token w in {0, 1} (stripe 0, owned by wavefront 0), shared
+// with the other wavefronts.
+template <int W>
+__device__ __forceinline__ int first_token_state(const ChainHead &h, const float *ls, const int *ln, int w,
+                                                 Exchange *xc, int &xi, int wave, int lane) {
+    int ns = 0;
+    if (wave == 0) {
+        float lm;
+        slot_value(h, ls[w], ln[w], lm, ns);
+    }
+    if (W > 1) {
+        const int buf = xi & 1;
+        ++xi;
+        if (wave == 0 && lane == 0) xc->payload[buf][0] = ns;
+        lds_barrier();
+        ns = __builtin_amdgcn_readfirstlane(xc->payload[buf][0]);
+    }
+    return ns;
+}
+
+// One fused greedy step of a hypothesis held by W wavefronts.  row: its V
+// token ASR log-probabilities in LDS (asr_row_words(V) words, owned stripes
+// landed unless ROW_PENDING, in which case their copy was issued just before);
+// rowV: class V (blank, or <eos> in AED mode).  s: valid state (uniform); pv:
+// previous label (CTC).  Returns the label and updates s; all lanes of all W
+// wavefronts return the same values.
+template <int MODE, int W, bool ROW_PENDING>
+__device__ __forceinline__ int greedy_step(const DevTrie &t, const float *row, float rowV, float lambda, int &s,
+                                           int pv, float *ls, int *ln, Exchange *xc, int &xi, int wave, int lane,
+                                           const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0) {
     const int V = t.vocab_size;
     const float fin = MODE == kAed ? t.final_w[s] : 0.0f;   // <eos> takes the state's final weight
     // The chain record is fetched first: in CTC and transducer modes its load
@@ -95,52 +169,68 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *row, f
     if (MODE == kCtc || MODE == kTransducer) {
         if (ROW_PENDING) wait_lds_copies();
         float bx = -__builtin_inff(), av;
-        int bi = kNone;
-        scan_row(row, V, lane, bx, bi);
-        int a = wave_argmax(bx, bi, av);
+        int bi = kNone, unused;
+        scan_row<W>(row, V, wave, lane, bx, bi);
+        int a = group_argmax<W>(bx, bi, 0, av, unused, xc, xi, wave, lane);
         if (a == kNone) a = 0;                    // every token at -inf: the first one, unless blank beats it
-        if (row[V] > av) a = V;                   // blank only when strictly larger (it has the highest index)
+        if (rowV > av) a = V;                     // blank only when strictly larger (it has the highest index)
         if (a == V || (MODE == kCtc && a == pv)) {   // blank or repeat: no LM, no move
-            if (pf_src) copy_to_lds_dword(pf_src, pf_dst, pf_n, lane);
+            if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
             return a;
         }
     }
-    const ChainHead h = walk_record(t, rec, nlev, ls, ln, lane, pf_src, pf_dst, pf_n);
+    const ChainHead h = walk_record<W>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
     float bx = -__builtin_inff(), wv;
     int bi = kNone;
-    scan_fused<MODE>(h, ls, ln, row, lambda, pv, V, lane, bx, bi);
-    int w = wave_argmax(bx, bi, wv);
-    if (w == kNone) w = (MODE == kCtc && pv == 0) ? 1 : 0;   // every candidate at -inf: the first one
-    if (MODE == kAed && __builtin_fmaf(lambda, fin, row[V]) > wv)
+    scan_fused<MODE, W>(h, ls, ln, row, lambda, pv, V, wave, lane, bx, bi);
+    // each lane's candidate next state rides along with its key (read from its own stripe)
+    int cand = 0;
+    if (bi != kNone) {
+        float lm;
+        slot_value(h, ls[bi], ln[bi], lm, cand);
+    }
+    int ns;
+    int w = group_argmax<W>(bx, bi, cand, wv, ns, xc, xi, wave, lane);
+    if (MODE == kAed && __builtin_fmaf(lambda, fin, rowV) > wv)
         return V;   // <eos> strictly above every token: the sentence ends, the state stays
-    float lm;
-    int n;
-    slot_value(h, ls[w], ln[w], lm, n);   // uniform w: every lane reads the same slot
-    s = n;
+    if (w == kNone) {   // every candidate at -inf: the first one
+        w = (MODE == kCtc && pv == 0) ? 1 : 0;
+        ns = first_token_state<W>(h, ls, ln, w, xc, xi, wave, lane);
+    }
+    s = ns;
     return w;
 }
 
-template <int HPB, int MODE>
-__global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, const float *__restrict__ asr,
-                                                                  int64_t B, int64_t ld, float lambda,
-                                                                  int32_t *__restrict__ states,
-                                                                  int32_t *__restrict__ prev,
-                                                                  int32_t *__restrict__ tokens) {
+// LDS of one hypothesis: the walked row (ls, ln), nrows ASR rows, the exchange area.
+__host__ __device__ inline size_t hyp_lds_bytes(int V, int nrows) {
+    return (2 * size_t(lds_row(V)) + size_t(nrows) * size_t(asr_row_words(V))) * sizeof(float) + sizeof(Exchange);
+}
+
+// One fused step; one hypothesis per workgroup of W wavefronts.
+template <int MODE, int W>
+__global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
+                                                                int64_t ld, float lambda,
+                                                                int32_t *__restrict__ states,
+                                                                int32_t *__restrict__ prev,
+                                                                int32_t *__restrict__ tokens) {
     extern __shared__ float lds[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
-    const int64_t b = int64_t(blockIdx.x) * HPB + wave;
+    const int64_t b = blockIdx.x;
     if (b >= B) return;
     const int V = t.vocab_size;
-    float *ls = lds + size_t(wave) * (2 * lds_row(V) + asr_row_words(V));
+    float *ls = lds;
     int *ln = reinterpret_cast<int *>(ls + lds_row(V));
     float *arow = reinterpret_cast<float *>(ln + lds_row(V));
+    Exchange *xc = reinterpret_cast<Exchange *>(arow + asr_row_words(V));
 
     // the ASR row's copy into LDS goes out with the state load
-    copy_to_lds_dword(asr + b * ld, arow, MODE == kPlain ? V : V + 1, lane);
+    const float *src = asr + b * ld;
+    copy_stripes_dword<W>(src, arow, V, wave, lane);
+    const float rowV = MODE == kPlain ? 0.0f : src[V];
     int s = __builtin_amdgcn_readfirstlane(states[b]);
     if (s < 0 || s >= t.num_states) {
-        if (lane == 0) {
+        if (wave == 0 && lane == 0) {
             atomicAdd(&t.status[0], 1);
             tokens[b] = -1;
         }
@@ -148,8 +238,11 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
         return;
     }
     const int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
-    const int label = greedy_step<MODE, true>(t, arow, lambda, s, pv, ls, ln, lane);
-    if (lane == 0) {
+    int xi = 0;
+    // every wavefront has read states[b] and prev[b] before the first exchange
+    // barrier inside the step, and wavefront 0 writes them back after it
+    const int label = greedy_step<MODE, W, true>(t, arow, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
+    if (wave == 0 && lane == 0) {
         tokens[b] = label;
         states[b] = s;
         if (MODE == kCtc) prev[b] = label;
@@ -157,17 +250,19 @@ __global__ __launch_bounds__(HPB * kWave) void fused_step_kernel(DevTrie t, cons
 }
 
 // Whole greedy decode: utterance b runs frames 0 .. len_b - 1 of
-// asr[b * stride_b + t * stride_t + class].
-template <int MODE>
-__global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
-                                                              int64_t T, int64_t stride_b, int64_t stride_t,
-                                                              const int32_t *__restrict__ lengths, float lambda,
-                                                              int32_t *__restrict__ states,
-                                                              int32_t *__restrict__ prev,
-                                                              int32_t *__restrict__ labels,
-                                                              int32_t *__restrict__ label_states) {
+// asr[b * stride_b + t * stride_t + class]; one utterance per workgroup of W
+// wavefronts.
+template <int MODE, int W>
+__global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
+                                                                  int64_t T, int64_t stride_b, int64_t stride_t,
+                                                                  const int32_t *__restrict__ lengths, float lambda,
+                                                                  int32_t *__restrict__ states,
+                                                                  int32_t *__restrict__ prev,
+                                                                  int32_t *__restrict__ labels,
+                                                                  int32_t *__restrict__ label_states) {
     extern __shared__ float lds[];
-    const int lane = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int lane = threadIdx.x % kWave;
     const int64_t b = blockIdx.x;
     if (b >= B) return;
     const int V = t.vocab_size;
@@ -175,6 +270,7 @@ __global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const fl
     float *ls = lds;
     int *ln = reinterpret_cast<int *>(ls + lds_row(V));
     float *abuf = reinterpret_cast<float *>(ln + lds_row(V));   // two ASR rows, double-buffered
+    Exchange *xc = reinterpret_cast<Exchange *>(abuf + 2 * rowp);
     int32_t *lab = labels + b * T;
     int32_t *lst = label_states ? label_states + b * T : nullptr;
 
@@ -185,38 +281,60 @@ __global__ __launch_bounds__(kWave) void fused_decode_kernel(DevTrie t, const fl
     }
     int s = __builtin_amdgcn_readfirstlane(states[b]);
     if (s < 0 || s >= t.num_states) {
-        if (lane == 0) atomicAdd(&t.status[0], 1);
-        for (int64_t f = lane; f < T; f += kWave) {
-            lab[f] = -1;
-            if (lst) lst[f] = -1;
+        if (wave == 0) {
+            if (lane == 0) atomicAdd(&t.status[0], 1);
+            for (int64_t f = lane; f < T; f += kWave) {
+                lab[f] = -1;
+                if (lst) lst[f] = -1;
+            }
         }
         return;
     }
     int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
     const float *row = asr + b * stride_b;
-    const int cn = MODE == kPlain ? V : V + 1;   // ASR row words used
-    if (len > 0) copy_to_lds_dword(row, abuf, cn, lane);
+    if (len > 0) copy_stripes_dword<W>(row, abuf, V, wave, lane);
+    float rowV = (MODE != kPlain && len > 0) ? row[V] : 0.0f;
+    int keep_lab = -1, keep_st = -1, xi = 0;
     for (int64_t f = 0; f < len; ++f, row += stride_t) {
         // frame f reads its ASR row from LDS, copied during frame f - 1 (or
         // before the loop); the walk also starts the copy of row f + 1
         wait_lds_copies();
         float *cur = abuf + (f & 1) * rowp;
         float *nxt = abuf + ((f + 1) & 1) * rowp;
-        const float *pf = f + 1 < len ? row + stride_t : nullptr;
-        const int label = greedy_step<MODE, false>(t, cur, lambda, s, pv, ls, ln, lane, pf, nxt, cn);
+        const bool more = f + 1 < len;
+        const float *pf = more ? row + stride_t : nullptr;
+        const float next_v = (MODE != kPlain && more) ? row[stride_t + V] : 0.0f;
+        const int label = greedy_step<MODE, W, false>(t, cur, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, pf,
+                                                      nxt, V);
+        rowV = next_v;
         if (MODE == kCtc) pv = label;
-        if (lane == 0) {
-            lab[f] = label;
-            if (lst) lst[f] = s;
+        // Lane f % 64 of wavefront 0 keeps frame f's label and state; one
+        // coalesced store per 64 frames, so the wait at the top of a frame
+        // rarely has a store to drain.
+        const int slot = int(f & (kWave - 1));
+        if (lane == slot) {
+            keep_lab = label;
+            keep_st = s;
+        }
+        if (wave == 0 && (slot == kWave - 1 || f + 1 == len)) {
+            const int64_t f0 = f - slot;
+            if (lane <= slot) {
+                lab[f0 + lane] = keep_lab;
+                if (lst) lst[f0 + lane] = keep_st;
+            }
         }
     }
-    for (int64_t f = len + lane; f < T; f += kWave) {   // frames past the utterance's end
-        lab[f] = -1;
-        if (lst) lst[f] = s;
-    }
-    if (lane == 0) {
-        states[b] = s;
-        if (MODE == kCtc) prev[b] = pv;
+    if (wave == 0) {
+        for (int64_t f = len + lane; f < T; f += kWave) {   // frames past the utterance's end
+            lab[f] = -1;
+            if (lst) lst[f] = s;
+        }
+        // every wavefront read states[b] and prev[b] before the first exchange
+        // barrier; with no frame at all the values written are the ones read
+        if (lane == 0) {
+            states[b] = s;
+            if (MODE == kCtc) prev[b] = pv;
+        }
     }
 }
 
@@ -304,37 +422,61 @@ hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int6
     return hipGetLastError();
 }
 
-template <int HPB, int MODE>
-static hipError_t launch_one(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
-                             int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
-    const int64_t blocks = (B + HPB - 1) / HPB;
-    const size_t lds =
-        size_t(HPB) * (2 * size_t(lds_row(t.vocab_size)) + size_t(asr_row_words(t.vocab_size))) * sizeof(float);
-    hipLaunchKernelGGL((fused_step_kernel<HPB, MODE>), dim3(unsigned(blocks)), dim3(HPB * kWave), lds, stream,
-                       t, asr, B, ld, lambda, states, prev, tokens);
+// Wavefronts per hypothesis: a batch of up to 512 hypotheses leaves most SIMDs
+// idle with one wavefront each, so each hypothesis gets four (measured on the
+// 20M 6-gram decode: 4-12 % less time per frame); from 1024 on, one wavefront
+// per hypothesis keeps more work in flight and wins.
+inline int waves_per_hyp(int64_t B) { return B <= 512 ? 4 : 1; }
+
+template <int MODE, int W>
+static hipError_t launch_step_w(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
+                                int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
+    hipLaunchKernelGGL((fused_step_kernel<MODE, W>), dim3(unsigned(B)), dim3(W * kWave),
+                       hyp_lds_bytes(t.vocab_size, 1), stream, t, asr, B, ld, lambda, states, prev, tokens);
     return hipGetLastError();
 }
 
-// One hypothesis per workgroup: a step batch is a few hundred hypotheses, so
-// spreading them over all CUs beats packing them.
+template <int MODE>
+static hipError_t launch_step_mode(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
+                                   int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
+    switch (waves_per_hyp(B)) {
+        case 4: return launch_step_w<MODE, 4>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        default: return launch_step_w<MODE, 1>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+    }
+}
+
 hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int64_t ld, int mode, float lambda,
                              int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
     switch (mode) {
-        case kPlain: return launch_one<1, kPlain>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        case kCtc: return launch_one<1, kCtc>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        case kAed: return launch_one<1, kAed>(t, asr, B, ld, lambda, states, prev, tokens, stream);
-        default: return launch_one<1, kTransducer>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        case kPlain: return launch_step_mode<kPlain>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        case kCtc: return launch_step_mode<kCtc>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        case kAed: return launch_step_mode<kAed>(t, asr, B, ld, lambda, states, prev, tokens, stream);
+        default: return launch_step_mode<kTransducer>(t, asr, B, ld, lambda, states, prev, tokens, stream);
     }
+}
+
+template <int MODE, int W>
+static hipError_t launch_decode_w(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
+                                  const int32_t *lengths, float lambda, int32_t *states, int32_t *prev,
+                                  int32_t *labels, int32_t *label_states, hipStream_t stream) {
+    hipLaunchKernelGGL((fused_decode_kernel<MODE, W>), dim3(unsigned(B)), dim3(W * kWave),
+                       hyp_lds_bytes(t.vocab_size, 2), stream, t, asr, B, T, sb, st, lengths, lambda, states, prev,
+                       labels, label_states);
+    return hipGetLastError();
 }
 
 template <int MODE>
 static hipError_t launch_decode_mode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb,
                                      int64_t st, const int32_t *lengths, float lambda, int32_t *states,
                                      int32_t *prev, int32_t *labels, int32_t *label_states, hipStream_t stream) {
-    const size_t lds = (2 * size_t(lds_row(t.vocab_size)) + 2 * size_t(asr_row_words(t.vocab_size))) * sizeof(float);
-    hipLaunchKernelGGL((fused_decode_kernel<MODE>), dim3(unsigned(B)), dim3(kWave), lds, stream, t, asr, B, T, sb,
-                       st, lengths, lambda, states, prev, labels, label_states);
-    return hipGetLastError();
+    switch (waves_per_hyp(B)) {
+        case 4:
+            return launch_decode_w<MODE, 4>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                            label_states, stream);
+        default:
+            return launch_decode_w<MODE, 1>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                            label_states, stream);
+    }
 }
 
 hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,

@@ -156,15 +156,64 @@ __device__ __forceinline__ int4 fetch_record(const DevTrie &t, int s, int lane, 
     return load_record(rp, nlev, lane);
 }
 
-// The walk of a fetched record into (ls, ln).  When pf_src is given, pf_n
-// words from it are also copied into pf_dst once the record is in (a prefetch
-// that rides along with the dense row and the arcs).
+// Token stripes: tokens [256c, 256c + 256) form stripe c.  When W wavefronts
+// share one hypothesis, wavefront w owns the stripes c with c % W == w: it
+// alone copies, writes and reads their LDS slots, so the wavefronts of a
+// hypothesis never touch each other's slots.  W = 1: one wavefront owns all.
+constexpr int kStripe = 256;
+
+template <int W>
+__device__ __forceinline__ bool owns_token(int tok, int wave) {
+    return W == 1 || ((tok >> 8) & (W - 1)) == wave;
+}
+
+// n words from src (global) into dst (LDS), the owned stripes only; dst padded
+// to whole stripes.
+template <int W>
+__device__ __forceinline__ void copy_stripes_dword(const void *src, void *dst, int n, int wave, int lane) {
+    if (W == 1) {
+        copy_to_lds_dword(src, dst, n, lane);
+        return;
+    }
+    const uint32_t *s = static_cast<const uint32_t *>(src);
+    uint32_t *d = static_cast<uint32_t *>(dst);
+    for (int c = kStripe * wave; c < n; c += kStripe * W)
+        copy_to_lds_dword(s + c, d + c, n - c < kStripe ? n - c : kStripe, lane);
+}
+
+template <int W>
+__device__ __forceinline__ void dense_stripes_to_lds(const DevTrie &t, int row, float *ls, int *ln, int wave,
+                                                     int lane) {
+    if (W == 1) {
+        dense_to_lds(t, row, ls, ln, lane);
+        return;
+    }
+    const int V = t.vocab_size;
+    const float *dw = t.dense_w + size_t(row) * V;
+    const int32_t *dt = t.dense_to + size_t(row) * V;
+    for (int c = kStripe * wave; c < V; c += kStripe * W) {
+        const int n = V - c < kStripe ? V - c : kStripe;
+        if ((V & 3) == 0) {
+            copy_to_lds_x4(dw + c, ls + c, n, lane);
+            copy_to_lds_x4(dt + c, ln + c, n, lane);
+        } else {
+            copy_to_lds_dword(dw + c, ls + c, n, lane);
+            copy_to_lds_dword(dt + c, ln + c, n, lane);
+        }
+    }
+}
+
+// The walk of a fetched record into (ls, ln), the stripes of wavefront `wave`
+// of W.  When pf_src is given, pf_n words from it are also copied into pf_dst
+// (the owned stripes) once the record is in (a prefetch that rides along with
+// the dense row and the arcs).
+template <int W = 1>
 __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
-                                                 int lane, const float *pf_src = nullptr, float *pf_dst = nullptr,
-                                                 int pf_n = 0) {
+                                                 int lane, int wave = 0, const float *pf_src = nullptr,
+                                                 float *pf_dst = nullptr, int pf_n = 0) {
     const ChainHead h = head_of(rec);
-    dense_to_lds(t, h.dense_row, ls, ln, lane);
-    if (pf_src) copy_to_lds_dword(pf_src, pf_dst, pf_n, lane);
+    dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
+    if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
     // levels bottom-up: entry nlev (order 2) first, entry 1 (the query state) last
     for (int j = nlev; j >= 1; --j) {
         const int begin = __builtin_amdgcn_readlane(rec.x, j);
@@ -173,6 +222,11 @@ __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &r
         for (int a0 = begin; a0 < end; a0 += kWave * kArcUnroll) {
             ArcStripe st;
             load_stripe(t, a0, end, lane, st);
+            if (W > 1) {
+#pragma unroll
+                for (int u = 0; u < kArcUnroll; ++u)
+                    if (!owns_token<W>(st.tok[u], wave)) st.tok[u] = -1;
+            }
             store_stripe(st, acc, ls, ln);
         }
     }

@@ -311,6 +311,25 @@ def test_decode_launch_modes_ragged_lengths(dev, mode):
     assert np.array_equal(fin, os_[:, -1])
 
 
+@pytest.mark.parametrize("B", [513, 1100])
+def test_fused_larger_batches(dev, B):
+    """Batches above 512 hypotheses, which run with one wavefront per hypothesis
+    instead of four."""
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    T = 16
+    starts = uniform_states(m, B, seed=B)
+    asr = asr_logprobs((B, T, V + 1), seed=B + 1, blank_boost=1.0)
+    lengths = np.random.default_rng(B + 2).integers(0, T + 1, B).astype(np.int32)
+    for mode in (MODE_PLAIN, MODE_CTC):
+        a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+        check_decode(f"B={B} mode={mode}", lm, o, a, mode, 0.5, starts, dev)
+        case(f"decode launch B={B} mode={mode} ragged")
+        gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev, lengths=lengths)
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS, lengths=lengths)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+
+
 def test_decode_launch_resumes_exactly(dev):
     """Two launches over frames [0, 40) and [40, 90), passing states and labels
     back, equal one decode over all 90 frames."""

@@ -17,6 +17,7 @@ second over the timed steps.  The same run also reports:
   one HIP graph;
 * the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame,
   and the same decode of 1000 frames as one launch;
+* the k best fused tokens (beam expansion) of 1024 hypotheses, k = 4 and 32;
 * plain fusion on the 200k-n-gram 4-gram at B = 32 hypotheses x 200 steps;
 * cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
   host cores.
@@ -276,6 +277,31 @@ def main():
         f"{fused_decode['frames_per_s']:.3g} frames/s")
     del asr, asr_bt
 
+    # ---- beam expansion on the 20M 6-gram: the k best fused tokens of 1024 hypotheses
+    Bk = 1024
+    kst = torch.from_numpy(uniform_states(model, Bk, seed=seed_for(5) + 9)).to(dev)
+    gk = torch.Generator(device=dev)
+    gk.manual_seed(seed_for(5) + 10)
+    kasr = torch.log_softmax(torch.randn((Bk, V), generator=gk, device=dev) * 3.0, dim=-1)
+    topk = {"workload": f"{Bk} hypotheses (256 utterances x beam 4), V={V}, 20M 6-gram, lambda={fspec.lam}"}
+    for kk in (4, 32):
+        ktok = torch.empty((Bk, kk), dtype=torch.int32, device=dev)
+        ksc = torch.empty((Bk, kk), dtype=torch.float32, device=dev)
+        knx = torch.empty((Bk, kk), dtype=torch.int32, device=dev)
+        for _ in range(5):
+            lm.fused_topk(kasr, fspec.lam, kk, kst, tokens=ktok, scores=ksc, next_states=knx)
+        torch.cuda.synchronize()
+        f0.record(stream)
+        for _ in range(50):
+            lm.fused_topk(kasr, fspec.lam, kk, kst, tokens=ktok, scores=ksc, next_states=knx)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        topk[f"k{kk}_us_per_call"] = f0.elapsed_time(f1) * 1e3 / 50
+    assert lm.check_states() == 0
+    log(f"fused top-k over {Bk} hypotheses: k=4 {topk['k4_us_per_call']:.1f} us, "
+        f"k=32 {topk['k32_us_per_call']:.1f} us per call")
+    del kasr
+
     # ---- plain fusion on the 200k 4-gram (config 2 shape): B = 32 hypotheses x 200 steps
     pspec = CONFIGS[2]
     pmodel = make_config_model(2)
@@ -355,6 +381,7 @@ def main():
         "fused": fused,
         "fused_decode": fused_decode,
         "fused_plain": fused_plain,
+        "fused_topk": topk,
         "advance_graph_b512": graph,
         "cpu_baseline": cpu,
         "kernel_source_sha256": kernel_source_hash(),

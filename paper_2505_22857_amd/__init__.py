@@ -260,17 +260,21 @@ class NgpuLM:
                                                _dptr(out, torch.float32, "out"), _stream_handle(stream)))
         return out
 
-    def fused_topk(self, asr, lam: float, k: int, states, stream=None):
-        """k best fused tokens per hypothesis: (tokens int32, scores fp32, next states int32), each [B, k]."""
+    def fused_topk(self, asr, lam: float, k: int, states, tokens=None, scores=None, next_states=None,
+                   stream=None):
+        """k best fused tokens per hypothesis: (tokens int32, scores fp32, next states int32), each [B, k]
+        (allocated unless given)."""
         import torch
         if asr.dim() != 2 or asr.stride(1) != 1 or asr.dtype != torch.float32 or not asr.is_cuda:
             raise TypeError("asr must be a float32 [B, ld] device tensor with unit stride in the last dimension")
         B = asr.shape[0]
         if states.numel() != B:
             raise ValueError("states must hold B entries")
-        tok = torch.empty((B, k), dtype=torch.int32, device=asr.device)
-        sc = torch.empty((B, k), dtype=torch.float32, device=asr.device)
-        nx = torch.empty((B, k), dtype=torch.int32, device=asr.device)
+        tok = torch.empty((B, k), dtype=torch.int32, device=asr.device) if tokens is None else tokens
+        sc = torch.empty((B, k), dtype=torch.float32, device=asr.device) if scores is None else scores
+        nx = torch.empty((B, k), dtype=torch.int32, device=asr.device) if next_states is None else next_states
+        if tok.numel() < B * k or sc.numel() < B * k or nx.numel() < B * k:
+            raise ValueError("output tensors are too small")
         _check(self._lib.ngpu_lm_fused_topk(self._h, ctypes.c_void_p(asr.data_ptr()), B, asr.stride(0), float(lam),
                                             int(k), _dptr(states, torch.int32, "states"),
                                             _dptr(tok, torch.int32, "tokens"), _dptr(sc, torch.float32, "scores"),

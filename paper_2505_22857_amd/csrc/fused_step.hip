@@ -339,9 +339,12 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
 }
 
 // The k best fused scores of one hypothesis per wavefront (beam-search
-// expansion): the row of fused values fmaf(lambda, lm[v], asr[v]) stays in
-// LDS, and k rounds of the wave argmax each take the best token not yet taken
-// (bit 31 of its next-state slot marks it).  Cost O(k V / 64) per wavefront.
+// expansion), in descending order with lowest-index ties.  After the walk,
+// each lane turns its slots into (fused value, next state) in place and keeps
+// its own best; a round reduces the lanes' bests to the winner (one DPP
+// reduction), and only the lane that held it marks the slot taken (bit 31 of
+// its next state), writes the outputs and rescans its own tokens.  Cost:
+// V / 64 per lane once, then k rounds of one reduction and one lane's rescan.
 __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                            int64_t ld, float lambda, int k,
                                                            const int32_t *__restrict__ states,
@@ -354,9 +357,11 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     const int V = t.vocab_size;
     float *ls = lds;
     int *ln = reinterpret_cast<int *>(ls + lds_row(V));
+    float *arow = reinterpret_cast<float *>(ln + lds_row(V));
     int32_t *otok = tokens + b * k;
     float *osc = scores + b * k;
     int32_t *onx = next + b * k;
+    copy_to_lds_dword(asr + b * ld, arow, V, lane);
     const int s = __builtin_amdgcn_readfirstlane(states[b]);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
@@ -365,31 +370,59 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
             osc[j] = NAN;
             onx[j] = -1;
         }
+        wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
-    const float *row = asr + b * ld;
-    for (int v = lane; v < V; v += kWave) {   // each lane rewrites only its own slots
-        float lm;
-        int n;
-        slot_value(h, ls[v], ln[v], lm, n);
-        ls[v] = __builtin_fmaf(lambda, lm, row[v]);
-        ln[v] = n;
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    constexpr int kTaken = int32_t(0x80000000u);
+    float bx = -__builtin_inff();
+    int bi = kNone;
+    for (int c = 0; c < V; c += kStripe) {   // lane l: tokens c + 4l .. c + 4l + 3, rewritten in place
+        const int v0 = c + 4 * lane;
+        f32x4 x = *reinterpret_cast<const f32x4 *>(ls + v0);
+        i32x4 n = *reinterpret_cast<const i32x4 *>(ln + v0);
+        const f32x4 a = *reinterpret_cast<const f32x4 *>(arow + v0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float lm;
+            int nx;
+            slot_value(h, x[j], n[j], lm, nx);
+            x[j] = __builtin_fmaf(lambda, lm, a[j]);
+            n[j] = v0 + j < V ? nx : kTaken;   // padding past V counts as taken
+            if (v0 + j < V) take_max(x[j], v0 + j, bx, bi);
+        }
+        *reinterpret_cast<f32x4 *>(ls + v0) = x;
+        *reinterpret_cast<i32x4 *>(ln + v0) = n;
     }
     for (int j = 0; j < k; ++j) {
-        unsigned long long best = 0;
-        for (int v = lane; v < V; v += kWave) {
-            if (ln[v] >= 0) {
-                const unsigned long long key = argmax_key(ls[v], v);
-                best = key > best ? key : best;
+        float wv;
+        int w = wave_argmax(bx, bi, wv);
+        if (w == kNone) {   // everything left is -inf: the lowest index not yet taken
+            int lo = kNone;
+            for (int c = 0; c < V && lo == kNone; c += kStripe) {
+                const int v0 = c + 4 * lane;
+                const i32x4 n = *reinterpret_cast<const i32x4 *>(ln + v0);
+#pragma unroll
+                for (int q = 3; q >= 0; --q)
+                    if (n[q] >= 0) lo = v0 + q;
             }
+            w = argmax_index(wave_max_u64(argmax_key(-__builtin_inff(), lo)));
         }
-        const int w = argmax_index(wave_max_u64(best));
-        if (lane == 0) {
+        if (lane == ((w & (kStripe - 1)) >> 2)) {   // the lane that owns token w
             otok[j] = w;
             osc[j] = ls[w];
             onx[j] = ln[w];
-            ln[w] = ln[w] | int32_t(0x80000000u);
+            ln[w] = ln[w] | kTaken;
+            bx = -__builtin_inff();
+            bi = kNone;
+            for (int c = 0; c < V; c += kStripe) {
+                const int v0 = c + 4 * lane;
+                const f32x4 x = *reinterpret_cast<const f32x4 *>(ls + v0);
+                const i32x4 n = *reinterpret_cast<const i32x4 *>(ln + v0);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (n[q] >= 0) take_max(x[q], v0 + q, bx, bi);
+            }
         }
     }
 }
@@ -416,7 +449,7 @@ hipError_t launch_final_weights(const DevTrie &t, const int32_t *states, int64_t
 hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
                              const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
                              hipStream_t stream) {
-    const size_t lds = 2 * size_t(lds_row(t.vocab_size)) * sizeof(float);
+    const size_t lds = (2 * size_t(lds_row(t.vocab_size)) + size_t(asr_row_words(t.vocab_size))) * sizeof(float);
     hipLaunchKernelGGL(fused_topk_kernel, dim3(unsigned(B)), dim3(kWave), lds, stream, t, asr, B, ld, lambda, k,
                        states, tokens, scores, next);
     return hipGetLastError();

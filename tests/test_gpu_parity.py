@@ -512,6 +512,37 @@ def test_fused_topk_cfg2(dev, k):
     assert np.abs(sc.cpu().numpy() - osc).max() <= TOL
 
 
+@pytest.mark.parametrize("lam", [0.0, 0.6])
+def test_fused_topk_minus_inf_and_ties(dev, lam):
+    m, lm, o = cfg_pair(2)
+    V = m.vocab_size
+    B, k = 8, 12
+    states = uniform_states(m, B, seed=61)
+    asr = asr_logprobs((B, V), seed=62)
+    asr[0] = -np.inf                                   # nothing finite: lowest indices in order
+    asr[1] = -np.inf                                   # three finite tokens, then the lowest untaken
+    asr[1, [900, 5, 300]] = [-1.0, -2.0, -3.0]
+    asr[2] = -7.0                                      # full ties
+    asr[3] = -9.0                                      # ties across lanes and stripes
+    asr[3, [260, 4, 256, 252, 1023, 767]] = 5.0
+    asr[4, :] = -np.inf                                # finite tokens fewer than k, spread over lanes
+    asr[4, ::97] = -0.5
+    case(f"fused top-k -inf rows and ties lambda={lam}")
+    tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), lam, k, torch.from_numpy(states).to(dev))
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    ot, osc, onx = o.fused_topk(asr, lam, k, states)
+    assert np.array_equal(tok.cpu().numpy(), ot)
+    assert np.array_equal(nx.cpu().numpy(), onx)
+    g = sc.cpu().numpy()
+    assert np.array_equal(np.isinf(g), np.isinf(osc))
+    fin = np.isfinite(osc)
+    assert np.abs(g[fin] - osc[fin]).max() <= TOL
+    assert ot[0].tolist() == list(range(k))
+    if lam == 0.0:
+        assert ot[3, :6].tolist() == [4, 252, 256, 260, 767, 1023]
+
+
 def test_fused_topk_odd_vocab_and_bad_state(dev):
     m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
     V = m.vocab_size

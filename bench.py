@@ -20,7 +20,8 @@ second over the timed steps.  The same run also reports:
 * the k best fused tokens (beam expansion) of 1024 hypotheses, k = 4 and 32;
 * plain fusion on the 200k-n-gram 4-gram at B = 32 hypotheses x 200 steps;
 * cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
-  host cores.
+  host cores; cpu_baseline_decode: the oracle on the whole CTC decode above,
+  with whether its labels equal the GPU decode's.
 """
 
 from __future__ import annotations
@@ -275,6 +276,8 @@ def main():
                     "us_per_step": dm * 1e3 / T}
     log(f"fused CTC decode in one launch: {dm:.2f} ms, {fused_decode['us_per_step']:.2f} us/step, "
         f"{fused_decode['frames_per_s']:.3g} frames/s")
+    asr_host = asr_bt.contiguous().cpu().numpy() if args.cpu_seconds > 0 else None   # for the oracle's decode
+    gpu_labels = labels.cpu().numpy()
     del asr, asr_bt
 
     # ---- beam expansion on the 20M 6-gram: the k best fused tokens of 1024 hypotheses
@@ -344,7 +347,7 @@ def main():
     del plm, pasr, pasr_bt
 
     # ---- CPU oracle on a bounded sample of the same workload
-    cpu = None
+    cpu = cpu_decode = None
     if args.cpu_seconds > 0:
         from oracle import Oracle
         cores = len(os.sched_getaffinity(0))
@@ -362,7 +365,17 @@ def main():
                "sample": f"{n} uniform states of the same model (the benchmark draw extended), "
                          f"full {V}-token rows, {dt:.1f}s"}
         log(f"oracle: {cpu['value']:.3g} scores/s on {cores} cores")
-        del o
+        # the whole config-5 CTC decode (same ASR tensor as the GPU decode above)
+        from oracle import MODE_CTC
+        t0 = time.perf_counter()
+        ol, _ = o.decode(asr_host, MODE_CTC, fspec.lam, np.zeros(Bf, np.int32), nthreads=cores)
+        dt = time.perf_counter() - t0
+        cpu_decode = {"value": Bf * T / dt, "unit": "utterance-frames/s", "cores": cores, "kind": "oracle",
+                      "sample": f"the whole CTC decode of {Bf} utterances x {T} frames, {dt:.1f}s",
+                      "labels_match_gpu": bool(np.array_equal(ol, gpu_labels))}
+        log(f"oracle CTC decode: {cpu_decode['value']:.3g} frames/s on {cores} cores, "
+            f"labels match the GPU decode: {cpu_decode['labels_match_gpu']}")
+        del o, asr_host
 
     out = {
         "metric": METRIC, "value": value, "unit": "scores/s", "n_gpus": 1, "steps": args.steps,
@@ -384,6 +397,7 @@ def main():
         "fused_topk": topk,
         "advance_graph_b512": graph,
         "cpu_baseline": cpu,
+        "cpu_baseline_decode": cpu_decode,
         "kernel_source_sha256": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)

@@ -99,10 +99,39 @@ def test_advance_cfg3_deep_phrase_states(dev):
     check_advance("cfg3 uniform", m, lm, o, uniform_states(m, 1000, seed=seed_for(3) + 1), dev)
 
 
-def test_advance_cfg4_batches_of_512(dev):
+def test_advance_cfg3_rows_normalised(dev):
+    """Every row of 10^5 sampled states sums to one (a property of the generated
+    model), on the GPU's scores."""
+    m, lm, o = cfg_pair(3)
+    st = np.concatenate([phrase_states(m, 20000, seed=seed_for(3) + 2),
+                         uniform_states(m, 80000, seed=seed_for(3) + 3)]).astype(np.int32)
+    case(f"advance cfg3 normalisation B={len(st)}")
+    sc, nx = lm.advance(torch.from_numpy(st).to(dev))
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    tot = torch.exp(sc.double()).sum(dim=1)
+    err = float((tot - 1).abs().max())
+    print(f"  cfg3 max |sum - 1| over {len(st)} rows: {err:.3g}", flush=True)
+    assert err < 1e-5
+    assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
+
+
+def test_advance_cfg4_64_batches_of_512(dev):
+    """64 independent 512-hypothesis calls, every row against the oracle."""
     m, lm, o = cfg_pair(4)
-    for r in range(8):
-        check_advance(f"cfg4 batch {r}", m, lm, o, uniform_states(m, 512, seed=seed_for(4) + r), dev)
+    R, Bb = 64, 512
+    states = np.concatenate([uniform_states(m, Bb, seed=seed_for(4) + r) for r in range(R)])
+    st = torch.from_numpy(states).to(dev)
+    sc = torch.empty((R * Bb, m.vocab_size), dtype=torch.float32, device=dev)
+    nx = torch.empty((R * Bb, m.vocab_size), dtype=torch.int32, device=dev)
+    case(f"advance cfg4 {R} calls of B={Bb}")
+    for r in range(R):
+        sl = slice(r * Bb, (r + 1) * Bb)
+        lm.advance(st[sl], sc[sl], nx[sl])
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
+    o_s32, o_nx, _ = o.advance(states, nthreads=NTHREADS)
+    assert_rows(f"cfg4 {R} x {Bb}", sc.cpu().numpy(), nx.cpu().numpy(), o_s32, o_nx)
 
 
 def test_advance_cfg4_bench_launch_sampled(dev):

@@ -21,7 +21,7 @@ import pytest
 import oracle
 from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle
 from oracle.bruteforce import BruteForce
-from synth import (asr_logprobs, generate_model, make_config_model, state_ids_of, tiny_model,
+from synth import (asr_logprobs, generate_model, make_config_model, phrase_states, state_ids_of, tiny_model,
                    uniform_states)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -205,6 +205,13 @@ def test_normalisation_config1_all_states(oracle_lib):
 def test_normalisation_config2_sampled(oracle_lib):
     model = make_config_model(2)
     check_normalisation(oracle.LIB_PATH, model, uniform_states(model, 3000, seed=9))
+
+
+def test_normalisation_config3_sampled(oracle_lib):
+    """The 2M 6-gram with context-biasing phrases: deep phrase states and uniform ones."""
+    model = make_config_model(3)
+    states = np.concatenate([phrase_states(model, 4000, seed=19), uniform_states(model, 16000, seed=20)])
+    check_normalisation(oracle.LIB_PATH, model, states.astype(np.int32))
 
 
 def test_normalisation_tiny_with_unk(oracle_lib):

@@ -252,6 +252,33 @@ def main():
              "us_per_step": f_ms * 1e3 / T}
     log(f"fused CTC: {fused['us_per_step']:.1f} us/step, {fused['frames_per_s']:.3g} frames/s")
 
+    # ---- the same per-frame launches replayed from one HIP graph (decoding steps in a graph)
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):             # warm the launch path on the capture stream
+            for t in range(3):
+                lm.fused_greedy_step(asr[t], fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, tokens=tok)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g_steps = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_steps):
+            for t in range(T):
+                lm.fused_greedy_step(asr[t], fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, tokens=tok)
+        g_ms = []
+        for _ in range(3):
+            fst.zero_()
+            prev.fill_(V)
+            f0.record(stream)
+            g_steps.replay()
+            f1.record(stream)
+            torch.cuda.synchronize()
+            g_ms.append(f0.elapsed_time(f1))
+        assert lm.check_states() == 0
+        fused["graph_us_per_step"] = float(np.median(g_ms)) * 1e3 / T
+        log(f"fused CTC, {T} per-frame launches in one graph: {fused['graph_us_per_step']:.2f} us/step")
+        del g_steps
+
     # ---- the same decode as one launch over all frames
     asr_bt = asr.permute(1, 0, 2)            # [B, T, C] view, unit class stride
     labels = torch.empty((Bf, T), dtype=torch.int32, device=dev)

@@ -1,17 +1,19 @@
 // Greedy shallow fusion (Section 2.3): one step over a batch of hypotheses, and
 // a whole decode over all frames of a batch of utterances in one launch.
 //
-// One wavefront per hypothesis.  CTC and transducer modes first take the plain
-// ASR argmax over the V + 1 classes; when that keeps blank (or, for CTC, the
-// previous label) the LM is not consulted at all and the state stays.
-// Otherwise the wavefront walks its state's backoff chain into an LDS row (the
-// same walk as the advance kernel, with no HBM write of the row), merges the
-// dense row of the order-1 ancestor, forms fmaf(lambda, lm[v], asr[v]) per
-// token and takes the argmax with lowest-index ties: each lane keeps a running
-// maximum over its tokens (read four at a time from LDS), then one 64-bit key
-// (value, ~index) per lane is reduced across the wavefront with DPP moves.
-// The winner's next state comes from the same merge.  No MFMA: one fma and one
-// compare per token.
+// One workgroup of W wavefronts per hypothesis (W = 4 for batches up to 512,
+// else 1), each wavefront owning every W-th stripe of 256 tokens.  CTC and
+// transducer modes first take the plain ASR argmax over the V + 1 classes;
+// when that keeps blank (or, for CTC, the previous label) the LM is not
+// consulted at all and the state stays.  Otherwise the workgroup walks its
+// state's backoff chain into an LDS row (the same walk as the advance kernel,
+// with no HBM write of the row), merges the dense row of the order-1 ancestor,
+// forms fmaf(lambda, lm[v], asr[v]) per token and takes the argmax with
+// lowest-index ties: each lane keeps a running maximum over its tokens (read
+// four at a time from LDS), one 64-bit key (value, ~index) per lane is reduced
+// across the wavefront with DPP moves, and the W wavefronts' winners meet in
+// one LDS exchange.  The winner's next state rides along with its key.  No
+// MFMA: one fma and one compare per token.
 //
 // The decode kernel keeps each utterance's state and previous label in
 // registers across frames: frame t + 1 depends on frame t only through them,
@@ -98,6 +100,7 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 template <int W>
 __device__ __forceinline__ int group_argmax(float bx, int bi, int payload, float &best, int &win_payload,
                                             Exchange *xc, int &xi, int wave, int lane) {
+    static_assert(W == 1 || W == 2 || W == 4, "the exchange area holds at most four wavefronts");
     const unsigned long long mine = argmax_key(bx, bi);
     unsigned long long k = wave_max_u64(mine);
     // the lane whose key won hands over its payload (the lowest such lane: keys are unique but for kNone)

@@ -41,7 +41,7 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
     int *ln = reinterpret_cast<int *>(ls + lds_row(V));
 
     // scan: lane i < G looks at hypothesis base + i
-    int s_l = -1;
+    int s_l = -1, dense_l = -1;
     bool mine = false;
     const int64_t bl = base + lane;
     if (lane < G && bl < B) {
@@ -55,6 +55,7 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
             int nl;
             const ChainHead hd = *reinterpret_cast<const ChainHead *>(chain_record(t, s_l, nl));
             mine = chain_group(hd) == grp;
+            dense_l = hd.dense_row;   // lets the walk start the dense-row copy before the record load
         }
     }
     uint64_t todo = __ballot(mine);
@@ -73,7 +74,9 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
             }
             continue;
         }
-        const ChainHead h = walk_into_lds(t, s, ls, ln, lane);
+        const ChainHead h = G == 1 ? walk_into_lds(t, s, ls, ln, lane)
+                                   : walk_into_lds_dense_first(t, s, __builtin_amdgcn_readlane(dense_l, i), ls,
+                                                               ln, lane);
         if (VEC) {
             for (int v = lane * 4; v < V; v += 4 * kWave) {
                 const int4 n4 = *reinterpret_cast<const int4 *>(ln + v);

@@ -244,6 +244,31 @@ __device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, floa
     return walk_record(t, rec, nlev, ls, ln, lane);
 }
 
+// The same walk when the state's dense row is already known (from its chain
+// head): the row's copy into LDS goes out before the record load, so the two
+// overlap instead of the copy waiting for the record.
+__device__ __forceinline__ ChainHead walk_into_lds_dense_first(const DevTrie &t, int s, int dense_row, float *ls,
+                                                               int *ln, int lane) {
+    dense_to_lds(t, dense_row, ls, ln, lane);
+    int nlev;
+    const int4 rec = fetch_record(t, s, lane, nlev);
+    const ChainHead h = head_of(rec);
+    // levels bottom-up, as in walk_record; the copy was issued before every arc
+    // load, so an arc's LDS write follows the copy's
+    for (int j = nlev; j >= 1; --j) {
+        const int begin = __builtin_amdgcn_readlane(rec.x, j);
+        const int end = __builtin_amdgcn_readlane(rec.y, j);
+        const float acc = __int_as_float(__builtin_amdgcn_readlane(rec.z, j));
+        for (int a0 = begin; a0 < end; a0 += kWave * kArcUnroll) {
+            ArcStripe st;
+            load_stripe(t, a0, end, lane, st);
+            store_stripe(st, acc, ls, ln);
+        }
+    }
+    wait_lds_copies();
+    return h;
+}
+
 // Final (score, next state) of one LDS slot.
 __device__ __forceinline__ void slot_value(const ChainHead &h, float x, int n, float &score, int &next) {
     if (n & kFinal) {

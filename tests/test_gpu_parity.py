@@ -155,16 +155,22 @@ def test_advance_cfg4_bench_launch_sampled(dev):
     assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
 
 
-@pytest.mark.parametrize("which", ["cfg2", "V1025"])
+@pytest.mark.parametrize("which", ["cfg2", "V1025", "N10"])
 def test_advance_grouped_mapping_with_bad_states(dev, which):
     """Batches of 32768 and more take the XCD-grouped mapping: every row, including
-    rows of out-of-range states (written by exactly one owner), vs the oracle."""
+    rows of out-of-range states (written by exactly one owner), vs the oracle.
+    N10: a 10-gram, whose order-9 states have chain records longer than the
+    scan preloads."""
     if which == "cfg2":
         m, lm, o = cfg_pair(2)
         B = 40000
-    else:
+    elif which == "V1025":
         m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
         B = 33001
+    else:
+        m, lm, o = pair("V16N10", lambda: generate_model(16, [16, 120, 200, 200, 180, 160, 140, 120, 100, 80],
+                                                          1.0, seed=26))
+        B = 32800
     states = uniform_states(m, B, seed=23)
     bad = np.random.default_rng(24).choice(B, 37, replace=False)
     states[bad[:20]] = -5

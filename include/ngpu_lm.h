@@ -98,7 +98,10 @@ typedef struct {
  * unigram gets unk_logprob and leads to state 0; pass NaN when every token has
  * a unigram), and per state its backoff weight and backoff state (its context
  * minus the first token).  An arc of order < N leads to the state of its own
- * n-gram, an arc of order N to the state of its last N-1 tokens.
+ * n-gram, an arc of order N to the state of its last N-1 tokens.  The image
+ * stores this as one record per state holding its whole backoff chain (arc
+ * ranges and the backoff weights already summed in Algorithm 1's order) and a
+ * dense V-wide row per order-1 context (layout in csrc/trie.h).
  * vocab_size: 1..NGPU_LM_MAX_VOCAB; additionally ceil(log2 V') * N <= 128 with
  * V' = V (V + 2 with NGPU_BUILD_BOS_EOS).
  * flags: 0 or NGPU_BUILD_BOS_EOS.  The list is read only during the call.

@@ -206,13 +206,15 @@ __device__ __forceinline__ void dense_stripes_to_lds(const DevTrie &t, int row, 
 // The walk of a fetched record into (ls, ln), the stripes of wavefront `wave`
 // of W.  When pf_src is given, pf_n words from it are also copied into pf_dst
 // (the owned stripes) once the record is in (a prefetch that rides along with
-// the dense row and the arcs).
-template <int W = 1>
+// the dense row and the arcs).  DENSE_ISSUED: the caller already issued the
+// copy of the dense row (before any arc load, which orders the arcs' LDS
+// writes after it).
+template <int W = 1, bool DENSE_ISSUED = false>
 __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
                                                  int lane, int wave = 0, const float *pf_src = nullptr,
                                                  float *pf_dst = nullptr, int pf_n = 0) {
     const ChainHead h = head_of(rec);
-    dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
+    if (!DENSE_ISSUED) dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
     if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
     // levels bottom-up: entry nlev (order 2) first, entry 1 (the query state) last
     for (int j = nlev; j >= 1; --j) {
@@ -252,21 +254,7 @@ __device__ __forceinline__ ChainHead walk_into_lds_dense_first(const DevTrie &t,
     dense_to_lds(t, dense_row, ls, ln, lane);
     int nlev;
     const int4 rec = fetch_record(t, s, lane, nlev);
-    const ChainHead h = head_of(rec);
-    // levels bottom-up, as in walk_record; the copy was issued before every arc
-    // load, so an arc's LDS write follows the copy's
-    for (int j = nlev; j >= 1; --j) {
-        const int begin = __builtin_amdgcn_readlane(rec.x, j);
-        const int end = __builtin_amdgcn_readlane(rec.y, j);
-        const float acc = __int_as_float(__builtin_amdgcn_readlane(rec.z, j));
-        for (int a0 = begin; a0 < end; a0 += kWave * kArcUnroll) {
-            ArcStripe st;
-            load_stripe(t, a0, end, lane, st);
-            store_stripe(st, acc, ls, ln);
-        }
-    }
-    wait_lds_copies();
-    return h;
+    return walk_record<1, true>(t, rec, nlev, ls, ln, lane);
 }
 
 // Final (score, next state) of one LDS slot.

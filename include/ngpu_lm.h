@@ -92,6 +92,17 @@ typedef struct {
  * </s>, an <unk> weight). */
 #define NGPU_BUILD_BOS_EOS 1u
 
+/* Build flag: close a list that is not closed (a pruned ARPA model) instead of
+ * rejecting it.  Every missing prefix and suffix of a listed n-gram (for an
+ * n-gram ending in </s>, its prefix) is inserted with backoff weight 0 and the
+ * weight the backoff rule of Section 2.1 gives it on the list without it; for
+ * an inserted c + v of order >= 2 that is B(c) + W(c[1:] + v) in one fp32 add
+ * (B(c) = 0 when c is inserted too), for an inserted unigram the <unk> weight
+ * (NGPU_E_MISSING_UNIGRAM without one).  The score of every token after every
+ * history is unchanged; the inserted contexts become states, so the state walk
+ * reaches the longest listed context of a history as the backoff rule does. */
+#define NGPU_BUILD_REPAIR_CLOSURE 2u
+
 /* Build the trie from a closed n-gram list (Section 2.2): states numbered
  * canonically, arcs sorted by (from_state, token) with one contiguous range per
  * state, a dense row over all V tokens for the empty context (a token without a
@@ -104,7 +115,9 @@ typedef struct {
  * dense V-wide row per order-1 context (layout in csrc/trie.h).
  * vocab_size: 1..NGPU_LM_MAX_VOCAB; additionally ceil(log2 V') * N <= 128 with
  * V' = V (V + 2 with NGPU_BUILD_BOS_EOS).
- * flags: 0 or NGPU_BUILD_BOS_EOS.  The list is read only during the call.
+ * flags: NGPU_BUILD_BOS_EOS and/or NGPU_BUILD_REPAIR_CLOSURE (else
+ * NGPU_E_MISSING_PREFIX / NGPU_E_MISSING_SUFFIX for a list that is not closed).
+ * The list is read only during the call.
  * On success *out holds a new handle (free with ngpu_lm_free). */
 int ngpu_lm_build(const ngpu_ngram_list *list, int32_t vocab_size, float unk_logprob,
                   uint32_t flags, ngpu_lm **out);

@@ -70,6 +70,11 @@ def load(path: str = LIB_PATH):
                                       vp, vp, vp, vp]
     lib.oracle_fused_topk.restype = ctypes.c_int
     lib.oracle_last_error.restype = ctypes.c_char_p
+    lib.oracle_repair.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, vp, vp, vp, vp, ctypes.c_float,
+                                  ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(vp),
+                                  ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp)]
+    lib.oracle_repair.restype = ctypes.c_int
+    lib.oracle_free_buffer.argtypes = [vp]
     _lib_cache[path] = lib
     return lib
 
@@ -82,6 +87,34 @@ class OracleError(RuntimeError):
     def __init__(self, code, msg=""):
         super().__init__(f"oracle error {code}: {msg}")
         self.code = code
+
+
+def repair_list(vocab_size, max_order, order, tokens, logprob, backoff, unk_logprob=float("nan"),
+                bos_eos: bool = False, lib_path: str = LIB_PATH):
+    """The closed list of a list that is not closed: the listed rows, then every
+    missing prefix and suffix with backoff 0 and the backoff rule's weight
+    (``oracle_repair``).  Returns (order, tokens, logprob, backoff)."""
+    lib = load(lib_path)
+    N = int(max_order)
+    order = np.ascontiguousarray(order, np.int32)
+    tokens = np.ascontiguousarray(tokens, np.int32).reshape(len(order), N)
+    logprob = np.ascontiguousarray(logprob, np.float32)
+    backoff = np.ascontiguousarray(backoff, np.float32)
+    m = ctypes.c_int64()
+    po, pt, pw, pb = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+    rc = lib.oracle_repair(int(vocab_size), N, len(order), _ptr(order), _ptr(tokens), _ptr(logprob), _ptr(backoff),
+                           float(unk_logprob), int(bool(bos_eos)), ctypes.byref(m), ctypes.byref(po),
+                           ctypes.byref(pt), ctypes.byref(pw), ctypes.byref(pb))
+    if rc != 0:
+        raise OracleError(rc, lib.oracle_last_error().decode())
+    n = int(m.value)
+    out = []
+    for p, ct, shape in ((po, ctypes.c_int32, (n,)), (pt, ctypes.c_int32, (n, N)), (pw, ctypes.c_float, (n,)),
+                         (pb, ctypes.c_float, (n,))):
+        arr = np.ctypeslib.as_array(ctypes.cast(p, ctypes.POINTER(ct)), shape=shape).copy()
+        lib.oracle_free_buffer(p)
+        out.append(arr)
+    return tuple(out)
 
 
 class Oracle:

@@ -33,10 +33,15 @@
  *                the AED mode adds class V = <eos>, scored with the LM's
  *                </s> weight of the state, and keeps the state when it wins.
  *                Ties go to the lowest index (strict '>' scan).
+ *   repair       a list that is not closed (a pruned model) is closed by
+ *                adding every missing prefix and suffix with backoff 0 and,
+ *                as weight, score(c, v) on the list without the added n-gram,
+ *                so that every history keeps its scores.
  *
  * Parity pins (no external implementation exists): hand-derived values on the
- * Figure 1 sentence, brute-force history recursion on tiny models, per-context
- * normalisation of generated models, and the N=1 / N=2 / lambda=0 reductions.
+ * Figure 1 sentence, brute-force history recursion on tiny models (and on
+ * pruned lists against the repaired ones), per-context normalisation of
+ * generated models, and the N=1 / N=2 / lambda=0 reductions.
  *
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared -pthread (no fused multiply-add
  * is formed anywhere except the explicit fmaf of the fusion rule).
@@ -251,6 +256,132 @@ static void score_one(const oracle_model *m, const int32_t *c, int n, int32_t v,
     *s64 = acc64 + (double)m->unk;
     *next = 0;
 }
+
+/* ---- closure repair (the definition behind the library's repair flag) ----
+ *
+ * A list that is not closed gets every missing prefix and suffix of a listed
+ * n-gram (for an n-gram ending in </s>, its prefix) added with backoff 0;
+ * added n-grams need their own prefixes and suffixes in turn, so the missing
+ * ones are collected from the highest order down.  Each added n-gram c + v
+ * then gets as weight the backoff rule's score of v after c on the list
+ * without it, computed order by order from 1 up on a model that holds the
+ * listed n-grams and the added ones of lower order.  An added unigram gets the
+ * <unk> weight. */
+
+typedef struct {
+    int64_t n, cap;
+    int32_t *ord, *tok;
+    float *W, *B;
+    char *added;
+    int N;
+} row_list;
+
+static int rl_push(row_list *l, int k, const int32_t *t, float w, float b, char added) {
+    if (l->n == l->cap) {
+        int64_t c = l->cap ? 2 * l->cap : 1024;
+        int32_t *o = (int32_t *)realloc(l->ord, sizeof(int32_t) * (size_t)c);
+        if (o) l->ord = o;
+        int32_t *tk = (int32_t *)realloc(l->tok, sizeof(int32_t) * (size_t)c * (size_t)l->N);
+        if (tk) l->tok = tk;
+        float *w2 = (float *)realloc(l->W, sizeof(float) * (size_t)c);
+        if (w2) l->W = w2;
+        float *b2 = (float *)realloc(l->B, sizeof(float) * (size_t)c);
+        if (b2) l->B = b2;
+        char *a2 = (char *)realloc(l->added, (size_t)c);
+        if (a2) l->added = a2;
+        if (!o || !tk || !w2 || !b2 || !a2) return OR_NOMEM;
+        l->cap = c;
+    }
+    l->ord[l->n] = k;
+    for (int i = 0; i < l->N; ++i) l->tok[l->n * l->N + i] = i < k ? t[i] : -1;
+    l->W[l->n] = w;
+    l->B[l->n] = b;
+    l->added[l->n] = added;
+    ++l->n;
+    return OR_OK;
+}
+
+/* A model over the rows of l that are listed, or added with order below kmax. */
+static int rl_model(const row_list *l, int32_t V, float unk, int flags, int kmax, oracle_model **m) {
+    row_list sub = {0, 0, NULL, NULL, NULL, NULL, NULL, l->N};
+    int rc = OR_OK;
+    for (int64_t r = 0; r < l->n && rc == OR_OK; ++r)
+        if (!l->added[r] || l->ord[r] < kmax)
+            rc = rl_push(&sub, l->ord[r], l->tok + r * l->N, l->W[r], l->B[r], 0);
+    if (rc == OR_OK) rc = oracle_create(V, l->N, sub.n, sub.ord, sub.tok, sub.W, sub.B, unk, flags, m);
+    free(sub.ord); free(sub.tok); free(sub.W); free(sub.B); free(sub.added);
+    return rc;
+}
+
+static int cmp_tuple_n;
+static int cmp_tuple(const void *a, const void *b) {
+    return memcmp(a, b, sizeof(int32_t) * (size_t)cmp_tuple_n);
+}
+
+int oracle_repair(int32_t V, int32_t N, int64_t M, const int32_t *order, const int32_t *tokens,
+                  const float *logprob, const float *backoff, float unk_logprob, int flags,
+                  int64_t *M_out, int32_t **order_out, int32_t **tokens_out, float **W_out, float **B_out) {
+    if (V <= 0 || N < 1 || N > ORACLE_MAX_ORDER || M < 0) { set_err("bad sizes"); return OR_BAD_ARG; }
+    const int special = flags & 1;
+    row_list l = {0, 0, NULL, NULL, NULL, NULL, NULL, N};
+    int rc = OR_OK;
+    for (int64_t r = 0; r < M && rc == OR_OK; ++r)
+        rc = rl_push(&l, order[r], tokens + r * N, logprob[r], backoff[r], 0);
+    /* collect: prefixes and suffixes of order k, from the top down */
+    for (int k = N; k >= 2 && rc == OR_OK; --k) {
+        oracle_model *m = NULL;
+        rc = rl_model(&l, V, unk_logprob, flags, ORACLE_MAX_ORDER + 1, &m);
+        if (rc != OR_OK) break;
+        int64_t nc = 0;
+        int32_t *cand = (int32_t *)malloc(sizeof(int32_t) * (size_t)(2 * l.n + 1) * (size_t)(k - 1));
+        if (!cand) { oracle_free(m); rc = OR_NOMEM; break; }
+        for (int64_t r = 0; r < l.n; ++r) {
+            if (l.ord[r] != k) continue;
+            const int32_t *t = l.tok + r * N;
+            memcpy(cand + nc++ * (k - 1), t, sizeof(int32_t) * (size_t)(k - 1));            /* prefix */
+            if (!(special && t[k - 1] == V + 1))
+                memcpy(cand + nc++ * (k - 1), t + 1, sizeof(int32_t) * (size_t)(k - 1));    /* suffix */
+        }
+        cmp_tuple_n = k - 1;
+        qsort(cand, (size_t)nc, sizeof(int32_t) * (size_t)(k - 1), cmp_tuple);
+        for (int64_t i = 0; i < nc && rc == OR_OK; ++i) {
+            const int32_t *c = cand + i * (k - 1);
+            if (i > 0 && memcmp(c, c - (k - 1), sizeof(int32_t) * (size_t)(k - 1)) == 0) continue;
+            if (lookup(m, c, k - 1) < 0) rc = rl_push(&l, k - 1, c, 0.0f, 0.0f, 1);
+        }
+        free(cand);
+        oracle_free(m);
+    }
+    /* weights: order by order from 1 up, by the backoff rule on the list without them */
+    for (int k = 1; k < N && rc == OR_OK; ++k) {
+        oracle_model *m = NULL;
+        rc = rl_model(&l, V, unk_logprob, flags, k, &m);
+        if (rc != OR_OK) break;
+        for (int64_t r = 0; r < l.n; ++r) {
+            if (!l.added[r] || l.ord[r] != k) continue;
+            if (k == 1 && isnan(unk_logprob)) { set_err("repair needs a unigram and no <unk>"); rc = OR_NO_UNK; break; }
+            float s32;
+            double s64;
+            int32_t nx;
+            score_one(m, l.tok + r * N, k - 1, l.tok[r * N + k - 1], &s32, &s64, &nx);
+            l.W[r] = s32;
+        }
+        oracle_free(m);
+    }
+    if (rc != OR_OK) {
+        free(l.ord); free(l.tok); free(l.W); free(l.B); free(l.added);
+        return rc;
+    }
+    free(l.added);
+    *M_out = l.n;
+    *order_out = l.ord;
+    *tokens_out = l.tok;
+    *W_out = l.W;
+    *B_out = l.B;
+    return OR_OK;
+}
+
+void oracle_free_buffer(void *p) { free(p); }
 
 /* Full row for state s: scores and next states of all V tokens. */
 static int score_row(const oracle_model *m, int64_t s, float *s32, double *s64, int32_t *next) {

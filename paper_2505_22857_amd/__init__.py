@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(HERE, "libngpu_lm.so")
 
 NGPU_FUSION_PLAIN, NGPU_FUSION_CTC, NGPU_FUSION_TRANSDUCER, NGPU_FUSION_AED = 0, 1, 2, 3
 NGPU_BUILD_BOS_EOS = 1
+NGPU_BUILD_REPAIR_CLOSURE = 2
 MAX_ORDER = 10
 MAX_VOCAB = 8192
 
@@ -159,7 +160,7 @@ class NgpuLM:
     """A trie built from an n-gram list (natural-log fp32 weights)."""
 
     def __init__(self, vocab_size: int, max_order: int, order, tokens, logprob, backoff,
-                 unk_logprob: float = float("nan"), bos_eos: bool = False):
+                 unk_logprob: float = float("nan"), bos_eos: bool = False, repair: bool = False):
         self._lib = load_library()
         self._h = None
         order = np.ascontiguousarray(order, np.int32)
@@ -170,7 +171,8 @@ class NgpuLM:
                          logprob.ctypes.data, backoff.ctypes.data)
         h = ctypes.c_void_p()
         _check(self._lib.ngpu_lm_build(ctypes.byref(lst), int(vocab_size), float(unk_logprob),
-                                       NGPU_BUILD_BOS_EOS if bos_eos else 0, ctypes.byref(h)))
+                                       (NGPU_BUILD_BOS_EOS if bos_eos else 0) |
+                                       (NGPU_BUILD_REPAIR_CLOSURE if repair else 0), ctypes.byref(h)))
         self._h = h
         info = _Info()
         _check(self._lib.ngpu_lm_info(h, ctypes.byref(info)))
@@ -334,4 +336,5 @@ class NgpuLM:
 
 
 __all__ = ["NgpuLM", "NgpuError", "load_library", "parse_arpa", "LIB_PATH", "EXPORTED", "NGPU_BUILD_BOS_EOS",
+           "NGPU_BUILD_REPAIR_CLOSURE",
            "NGPU_FUSION_PLAIN", "NGPU_FUSION_CTC", "NGPU_FUSION_TRANSDUCER", "NGPU_FUSION_AED"]

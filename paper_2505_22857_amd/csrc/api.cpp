@@ -87,7 +87,8 @@ int ngpu_lm_build(const ngpu_ngram_list *list, int32_t vocab_size, float unk_log
     if (!out) return fail(NGPU_E_INVALID_ARG, "out is null");
     *out = nullptr;
     if (!list) return fail(NGPU_E_INVALID_ARG, "list is null");
-    if ((flags & ~NGPU_BUILD_BOS_EOS) != 0) return fail(NGPU_E_INVALID_ARG, "unknown build flags");
+    if ((flags & ~(NGPU_BUILD_BOS_EOS | NGPU_BUILD_REPAIR_CLOSURE)) != 0)
+        return fail(NGPU_E_INVALID_ARG, "unknown build flags");
     ngpu_lm *lm = new (std::nothrow) ngpu_lm();
     if (!lm) return fail(NGPU_E_NO_MEMORY, "handle allocation failed");
     std::string err;

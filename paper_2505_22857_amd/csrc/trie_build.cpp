@@ -1,4 +1,5 @@
-// Host construction of the trie image from a closed n-gram list (Section 2.2).
+// Host construction of the trie image from a closed n-gram list (Section 2.2);
+// with NGPU_BUILD_REPAIR_CLOSURE a list that is not closed is closed first.
 //
 // Every n-gram is packed into a 128-bit key, ceil(log2 V) bits per token with
 // the first token most significant, so that numeric order of keys of one order
@@ -56,6 +57,89 @@ std::string tuple_text(u128 key, int k, int bits) {
         s += std::to_string(t);
     }
     return s + ")";
+}
+
+// Closure repair (NGPU_BUILD_REPAIR_CLOSURE): every missing prefix and suffix
+// of a listed n-gram (for n-grams ending in </s>, the prefix only) is inserted
+// with backoff 0 and the weight the backoff rule gives it on the list without
+// it.  Missing n-grams are collected from the highest order down (an inserted
+// n-gram needs its own prefix and suffix), then weighted from order 1 up:
+// for an inserted x = c + v of order k >= 2 the rule stops at the suffix x[1:],
+// which is present, so W(x) = B(c) + W(x[1:]) (one fp32 add, B(c) = 0 when c
+// was inserted too); an inserted unigram takes the <unk> weight.  Scores of
+// every history are unchanged (the rule adds B = 0 for an unlisted context),
+// and the inserted contexts become states the walk can reach.
+int repair_closure(std::vector<OrderLevel> &lv, int N, int bits, bool has_unk, float unk,
+                   const std::vector<std::pair<u128, int>> &final_ctx, std::string *err, int64_t *inserted) {
+    std::vector<std::vector<char>> ins(N + 1);
+    for (int k = 1; k <= N; ++k) ins[k].assign(lv[k].key.size(), 0);
+    *inserted = 0;
+    for (int k = N; k >= 1; --k) {
+        // missing (k-1)-grams: prefixes and suffixes of order-k n-grams, prefixes (contexts) of finals of order k
+        std::vector<u128> need;
+        if (k >= 2) {
+            const u128 smask = (u128(1) << (bits * (k - 1))) - 1;
+            for (const u128 &x : lv[k].key) {
+                need.push_back(x >> bits);
+                need.push_back(x & smask);
+            }
+        }
+        for (const auto &f : final_ctx)
+            if (f.second == k - 1 && k >= 2) need.push_back(f.first);
+        if (k == 1) break;
+        std::sort(need.begin(), need.end());
+        need.erase(std::unique(need.begin(), need.end()), need.end());
+        OrderLevel &L = lv[k - 1];
+        std::vector<u128> add;
+        for (const u128 &x : need)
+            if (!std::binary_search(L.key.begin(), L.key.end(), x)) add.push_back(x);
+        if (add.empty()) continue;
+        // merge the additions into the sorted level, weights filled in below
+        const size_t n0 = L.key.size(), n1 = n0 + add.size();
+        std::vector<u128> key(n1);
+        std::vector<float> w(n1), b(n1);
+        std::vector<char> mark(n1);
+        size_t i = 0, j = 0;
+        for (size_t p = 0; p < n1; ++p) {
+            if (j >= add.size() || (i < n0 && L.key[i] < add[j])) {
+                key[p] = L.key[i];
+                w[p] = L.w[i];
+                b[p] = L.b[i];
+                mark[p] = ins[k - 1][i];
+                ++i;
+            } else {
+                key[p] = add[j];
+                w[p] = 0.0f;
+                b[p] = 0.0f;
+                mark[p] = 1;
+                ++j;
+            }
+        }
+        L.key.swap(key);
+        L.w.swap(w);
+        L.b.swap(b);
+        ins[k - 1].swap(mark);
+        *inserted += int64_t(add.size());
+    }
+    for (int k = 1; k <= N; ++k) {
+        OrderLevel &L = lv[k];
+        const u128 smask = (u128(1) << (bits * (k - 1))) - 1;
+        for (size_t p = 0; p < L.key.size(); ++p) {
+            if (!ins[k][p]) continue;
+            if (k == 1) {
+                if (!has_unk) {
+                    *err = "repair needs the unigram " + tuple_text(L.key[p], 1, bits) + " but no <unk> weight was given";
+                    return NGPU_E_MISSING_UNIGRAM;
+                }
+                L.w[p] = unk;
+                continue;
+            }
+            const int64_t pr = find_rank(lv[k - 1].key, L.key[p] >> bits);
+            const int64_t sr = find_rank(lv[k - 1].key, L.key[p] & smask);
+            L.w[p] = lv[k - 1].b[size_t(pr)] + lv[k - 1].w[size_t(sr)];
+        }
+    }
+    return NGPU_OK;
 }
 
 }  // namespace
@@ -155,6 +239,14 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
             L.b[p] = k < N ? list->backoff[e[p].row] : 0.0f;
         }
         std::vector<Entry>().swap(e);
+    }
+    if (flags & NGPU_BUILD_REPAIR_CLOSURE) {
+        std::vector<std::pair<u128, int>> final_ctx;
+        for (const Final &f : finals)
+            if (f.order > 0) final_ctx.push_back({f.ctx, f.order});
+        int64_t added = 0;
+        const int rc = repair_closure(lv, N, bits, has_unk, unk, final_ctx, err, &added);
+        if (rc != NGPU_OK) return rc;
     }
     {
         int64_t regular = 0;   // unigrams of scored tokens (not <s>)

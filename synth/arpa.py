@@ -47,3 +47,29 @@ def write_arpa(model: NgramModel, vocab: Sequence[str]) -> str:
 def bpe_like_vocab(V: int):
     """V distinct word strings shaped like subword units."""
     return [f"▁w{i}" if i % 3 == 0 else f"t{i}" for i in range(V)]
+
+
+def write_arpa_list(V: int, N: int, order, tokens, logprob, backoff, unk_logprob, vocab: Sequence[str],
+                    bos_eos: bool = False) -> str:
+    """ARPA text of an n-gram list in any order (natural-log weights), e.g. a
+    pruned list that is not closed; rows are written per order as given."""
+    words = list(vocab) + (["<s>", "</s>"] if bos_eos else [])
+    order = np.asarray(order)
+    has_unk = not np.isnan(unk_logprob)
+    counts = [int((order == k).sum()) for k in range(1, N + 1)]
+    if has_unk:
+        counts[0] += 1
+    out = ["", "\\data\\"]
+    out += [f"ngram {k}={counts[k - 1]}" for k in range(1, N + 1)]
+    for k in range(1, N + 1):
+        out += ["", f"\\{k}-grams:"]
+        if k == 1 and has_unk:
+            out.append(f"{float(unk_logprob) / LN10!r}\t<unk>\t0")
+        for i in np.flatnonzero(order == k):
+            toks = [int(t) for t in tokens[i][:k]]
+            line = f"{float(logprob[i]) / LN10!r}\t{' '.join(words[t] for t in toks)}"
+            if k < N and not (bos_eos and toks[-1] == V + 1):
+                line += f"\t{float(backoff[i]) / LN10!r}"
+            out.append(line)
+    out += ["", "\\end\\", ""]
+    return "\n".join(out)

@@ -74,3 +74,19 @@ def tiny_model(V: int, N: int, seed: int, fill: float = 0.5, n_unigrams: Optiona
         counts.append(c)
         prev_count = c
     return generate_model(V, counts, zipf_s, seed)
+
+
+def pruned_list(model: NgramModel, drop: float, seed: int, drop_unigrams: int = 0):
+    """The model's n-gram list with a random fraction `drop` of the n-grams of
+    orders 2 .. N-1 removed (and `drop_unigrams` unigrams, for models with an
+    <unk> weight): a list that is not closed, as a pruned ARPA model can be.
+    Returns (order, tokens, logprob, backoff)."""
+    o, t, W, B = model.to_list()
+    rng = np.random.default_rng(seed)
+    keep = np.ones(len(o), bool)
+    mid = np.flatnonzero((o >= 2) & (o < model.max_order))
+    keep[rng.choice(mid, int(drop * len(mid)), replace=False)] = False
+    if drop_unigrams:
+        uni = np.flatnonzero((o == 1) & (t[:, 0] < model.vocab_size))
+        keep[rng.choice(uni, drop_unigrams, replace=False)] = False
+    return o[keep], t[keep], W[keep], B[keep]

@@ -197,6 +197,31 @@ def test_advance_odd_shapes(dev, V, N):
     check_advance(f"V={V} N={N}", m, lm, o, st, dev)
 
 
+def test_repaired_pruned_model(dev):
+    """A pruned (not closed) 4-gram built with closure repair: advance and the
+    decode launch against the oracle on the oracle's own repair of the list."""
+    from oracle import repair_list
+    from synth import pruned_list
+    m0 = make_config_model(2)
+    o, t, W, B = pruned_list(m0, 0.2, seed=11)
+    V, N = m0.vocab_size, m0.max_order
+    lm = ng.NgpuLM(V, N, o, t, W, B, m0.unk_logprob, repair=True).upload(dev)
+    R = repair_list(V, N, o, t, W, B, m0.unk_logprob)
+    orc = Oracle(V, N, *R, m0.unk_logprob)
+    assert lm.num_states == orc.num_states
+    states = np.concatenate([np.arange(0, lm.num_states, 37), [lm.num_states - 1]]).astype(np.int32)
+    check_advance("repaired pruned cfg2", None, lm, orc, states, dev)
+    Bq, T = 48, 40
+    starts = np.random.default_rng(13).integers(0, lm.num_states, Bq).astype(np.int32)
+    asr = asr_logprobs((Bq, T, V + 1), seed=14, blank_boost=1.0)
+    for mode in (MODE_PLAIN, MODE_CTC):
+        a = asr if mode == MODE_CTC else np.ascontiguousarray(asr[:, :, :V])
+        case(f"repaired pruned cfg2 decode launch mode={mode}")
+        gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
+        ol, os_ = orc.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+
+
 def test_advance_unigram_and_unk_models(dev):
     m, lm, o = pair("n1", lambda: generate_model(77, [77], 1.0, seed=2))
     check_advance("N=1", m, lm, o, np.zeros(5, np.int32), dev)

@@ -251,7 +251,8 @@ def test_build_error_codes():
     Wn = W.copy(); Wn[2] = np.nan
     assert _raw_build(3, 3, o, t, Wn, B)[0] == -10
     assert _raw_build(ng.MAX_VOCAB + 1, 3, o, t, W, B)[0] == -11
-    assert _raw_build(3, 3, o, t, W, B, flags=2)[0] == -1
+    assert _raw_build(3, 3, o, t, W, B, flags=4)[0] == -1          # unknown flag
+    assert _raw_build(3, 3, o, t, W, B, flags=2)[0] == 0           # closure repair of a closed list
 
 
 def test_queries_before_upload_fail_cleanly():

@@ -19,7 +19,8 @@ import pytest
 import oracle
 import paper_2505_22857_amd as ng
 from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, Oracle
-from synth import asr_logprobs, bpe_like_vocab, generate_model, make_config_model, tiny_model, write_arpa
+from synth import (asr_logprobs, bpe_like_vocab, generate_model, make_config_model, pruned_list, tiny_model,
+                   write_arpa)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -89,6 +90,19 @@ def test_builder_clean_and_identical(drivers, name):
     _write_list(lst, m.vocab_size, m.max_order, o, t, W, B, m.unk_logprob, flags)
     assert _run([bd, "list", lst, img]).split() == ["rc", "0"]
     ref = ng.NgpuLM(m.vocab_size, m.max_order, o, t, W, B, m.unk_logprob, bos_eos=m.bos_eos).host_image()
+    assert np.array_equal(np.fromfile(img, np.uint8), ref)
+
+
+@pytest.mark.parametrize("seed", [6, 7])
+def test_builder_repair_clean_and_identical(drivers, seed):
+    """A pruned list built with closure repair (flag 2)."""
+    bd, _, d = drivers
+    m = generate_model(8, [8, 40, 90, 100], 1.0, seed=seed)
+    o, t, W, B = pruned_list(m, 0.35, seed=seed + 100)
+    lst, img = str(d / f"pruned{seed}.list"), str(d / f"pruned{seed}.img")
+    _write_list(lst, 8, 4, o, t, W, B, m.unk_logprob, 2)
+    assert _run([bd, "list", lst, img]).split() == ["rc", "0"]
+    ref = ng.NgpuLM(8, 4, o, t, W, B, m.unk_logprob, repair=True).host_image()
     assert np.array_equal(np.fromfile(img, np.uint8), ref)
 
 

@@ -21,7 +21,8 @@ import pytest
 import oracle
 from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle
 from oracle.bruteforce import BruteForce
-from synth import (asr_logprobs, generate_model, make_config_model, phrase_states, state_ids_of, tiny_model,
+from synth import (asr_logprobs, generate_model, make_config_model, phrase_states, pruned_list, state_ids_of,
+                   tiny_model,
                    uniform_states)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -152,6 +153,44 @@ def check_ctc_rules(lib_path):
     assert tok[0] == V and st[0] == 0
     tok = o.greedy_step(np.array([[-1.2, -1.0, -3, -3, -3, -4]], np.float32), MODE_TRANSDUCER, lam, st)
     assert tok[0] == 0 and st[0] == 1
+
+
+def check_repair(lib_path, seeds=(6, 7)):
+    """Closure repair of pruned lists: the repaired list is closed, adds only
+    rows with backoff 0, and its state walk scores every token after every
+    history exactly as the backoff rule does on the pruned list (brute force
+    on histories); its states are the longest listed contexts of the repaired
+    list."""
+    for seed in seeds:
+        V, N = 8, 4
+        m = generate_model(V, [V, 40, 90, 100], 1.0, seed=seed)
+        o, t, W, B = pruned_list(m, 0.35, seed=seed + 100)
+        ro, rt, rW, rB = oracle.repair_list(V, N, o, t, W, B, m.unk_logprob, lib_path=lib_path)
+        rows = {tuple(int(x) for x in rt[i, :ro[i]]): (rW[i], rB[i]) for i in range(len(ro))}
+        given = {tuple(int(x) for x in t[i, :o[i]]): (W[i], B[i]) for i in range(len(o))}
+        assert len(rows) == len(ro)
+        for g, wb in given.items():
+            assert rows[g] == wb
+        for g, (w, b) in rows.items():
+            if g not in given:
+                assert b == 0.0 and np.isfinite(w)
+            if len(g) >= 2:
+                assert g[:-1] in rows and g[1:] in rows
+        bf = BruteForce(V, N, o, t, W, B, m.unk_logprob)
+        bf_rep = BruteForce(V, N, ro, rt, rW, rB, m.unk_logprob)
+        orc = Oracle(V, N, ro, rt, rW, rB, m.unk_logprob, lib_path=lib_path)
+        level = [((), 0)]
+        for L in range(N + 1):
+            sts = np.array([st for _, st in level], np.int32)
+            _, nx, s64 = orc.advance(sts, want64=True)
+            nxt = []
+            for i, (h, st) in enumerate(level):
+                assert orc.state_context(st) == bf_rep.state_context(h)
+                for v in range(V):
+                    assert abs(s64[i, v] - bf.score(h, v)) < 1e-5, (seed, h, v)
+                    if L < N:
+                        nxt.append((h + (v,), int(nx[i, v])))
+            level = nxt
 
 
 def check_generator_ids(lib_path):
@@ -435,6 +474,10 @@ def test_aed_mode_rules(oracle_lib):
         assert tok[b] == int(np.argmax(f)) or abs(f.max() - f[tok[b]]) < 1e-6
 
 
+def test_repair_of_pruned_lists(oracle_lib):
+    check_repair(oracle.LIB_PATH)
+
+
 def test_generator_and_oracle_number_states_alike(oracle_lib):
     check_generator_ids(oracle.LIB_PATH)
 
@@ -469,6 +512,8 @@ MUTANTS = {
     "repeat rescored": ("if (a == V || (mode == MODE_CTC && a == *prev)) {", "if (a == V) {"),
     "last index wins ties": ("if (best < 0 || f > bestval) { best = v; bestval = f; }",
                              "if (best < 0 || f >= bestval) { best = v; bestval = f; }"),
+    "repair weighs an added n-gram with itself": ("if (!l->added[r] || l->ord[r] < kmax)", "if (1)"),
+    "repair adds no suffixes": ("if (!(special && t[k - 1] == V + 1))\n", "if (0)\n"),
 }
 
 
@@ -491,6 +536,7 @@ def test_planted_mistake_is_caught(name, tmp_path):
         lambda: check_lambda_zero_and_ties(lib),
         lambda: check_ctc_rules(lib),
         lambda: check_generator_ids(lib),
+        lambda: check_repair(lib, seeds=(6,)),
     ]
     caught = 0
     for chk in checks:

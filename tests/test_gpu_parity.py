@@ -197,6 +197,32 @@ def test_advance_odd_shapes(dev, V, N):
     check_advance(f"V={V} N={N}", m, lm, o, st, dev)
 
 
+def ten_gram_pair():
+    return pair("V1024N10", lambda: generate_model(
+        1024, [1024, 20000, 40000, 40000, 30000, 20000, 15000, 10000, 8000, 6000], 1.0, seed=1010))
+
+
+def test_ten_gram_vocab_1024(dev):
+    """A 10-gram over V = 1024, the order and vocabulary of the paper's LMs:
+    chains of up to nine records, in the plain and the XCD-grouped mapping,
+    and the decode launch."""
+    m, lm, o = ten_gram_pair()
+    small = uniform_states(m, 3000, seed=101)
+    check_advance("10-gram plain mapping", m, lm, o, small, dev)
+    big = uniform_states(m, 40000, seed=102)
+    rows = np.random.default_rng(103).choice(len(big), 3000, replace=False)
+    check_advance("10-gram grouped mapping", m, lm, o, big, dev, rows=rows)
+    Bq, T = 64, 60
+    asr = asr_logprobs((Bq, T, 1025), seed=104, blank_boost=1.0)
+    starts = uniform_states(m, Bq, seed=105)
+    for mode in (MODE_PLAIN, MODE_CTC):
+        a = asr if mode == MODE_CTC else np.ascontiguousarray(asr[:, :, :1024])
+        case(f"10-gram decode launch mode={mode}")
+        gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
+        assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+
+
 def test_repaired_pruned_model(dev):
     """A pruned (not closed) 4-gram built with closure repair: advance and the
     decode launch against the oracle on the oracle's own repair of the list."""

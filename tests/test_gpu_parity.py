@@ -746,6 +746,25 @@ def test_graph_capture_replays_match_eager(dev):
     assert np.array_equal(ref[0].cpu().numpy().T, ol)
 
 
+def test_fused_zero_sizes(dev):
+    """B = 0 (and T = 0 for the decode) launch nothing and change nothing."""
+    m, lm, o = cfg_pair(1)
+    V = m.vocab_size
+    case("fused entry points with B = 0 / T = 0")
+    empty_asr = torch.empty((0, V + 1), device=dev)
+    st0 = torch.empty(0, dtype=torch.int32, device=dev)
+    assert lm.fused_greedy_step(empty_asr, 0.5, st0, mode=ng.NGPU_FUSION_CTC,
+                                prev=torch.empty(0, dtype=torch.int32, device=dev)).numel() == 0
+    tok, sc, nx = lm.fused_topk(torch.empty((0, V), device=dev), 0.5, 3, st0)
+    assert tok.shape == (0, 3) and sc.shape == (0, 3) and nx.shape == (0, 3)
+    st = torch.tensor([3, 5], dtype=torch.int32, device=dev)
+    prev = torch.full((2,), V, dtype=torch.int32, device=dev)
+    lab = lm.fused_greedy_decode(torch.empty((2, 0, V + 1), device=dev), 0.5, st, prev, mode=ng.NGPU_FUSION_CTC)
+    torch.cuda.synchronize()
+    assert lab.shape == (2, 0) and st.tolist() == [3, 5] and prev.tolist() == [V, V]
+    assert lm.check_states() == 0
+
+
 def test_fused_out_of_range_state(dev):
     m, lm, o = cfg_pair(1)
     V = m.vocab_size

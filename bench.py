@@ -17,6 +17,9 @@ second over the timed steps.  The same run also reports:
   one HIP graph;
 * the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame,
   and the same decode of 1000 frames as one launch;
+* the same decode at B = 4096 utterances x 200 frames, with its algorithmic
+  HBM bytes (ASR rows, and chain records and arcs on the frames that consult
+  the LM);
 * the k best fused tokens (beam expansion) of 1024 hypotheses, k = 4 and 32;
 * plain fusion on the 200k-n-gram 4-gram at B = 32 hypotheses x 200 steps;
 * cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
@@ -303,6 +306,48 @@ def main():
                     "us_per_step": dm * 1e3 / T}
     log(f"fused CTC decode in one launch: {dm:.2f} ms, {fused_decode['us_per_step']:.2f} us/step, "
         f"{fused_decode['frames_per_s']:.3g} frames/s")
+    # ---- a large batch: 4096 utterances x 200 frames, where the decode is bandwidth-bound
+    Bl, Tl = 4096, 200
+    gl_ = torch.Generator(device=dev)
+    gl_.manual_seed(seed_for(5) + 20)
+    lasr = torch.log_softmax(torch.randn((Bl, Tl, V + 1), generator=gl_, device=dev) * 3.0
+                             + torch.nn.functional.one_hot(torch.tensor(V, device=dev), V + 1) * fspec.blank_boost,
+                             dim=-1)
+    lst_ = torch.zeros(Bl, dtype=torch.int32, device=dev)
+    lprev = torch.full((Bl,), V, dtype=torch.int32, device=dev)
+    llab = torch.empty((Bl, Tl), dtype=torch.int32, device=dev)
+    lls = torch.empty((Bl, Tl), dtype=torch.int32, device=dev)
+    lm.fused_greedy_decode(lasr, fspec.lam, lst_, lprev, mode=ng.NGPU_FUSION_CTC, labels=llab, label_states=lls)
+    l_ms = []
+    for _ in range(3):
+        lst_.zero_()
+        lprev.fill_(V)
+        f0.record(stream)
+        lm.fused_greedy_decode(lasr, fspec.lam, lst_, lprev, mode=ng.NGPU_FUSION_CTC, labels=llab,
+                               label_states=lls)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        l_ms.append(f0.elapsed_time(f1))
+    assert lm.check_states() == 0
+    lm_ms = float(np.median(l_ms))
+    # algorithmic HBM bytes: every frame's ASR row, plus on frames that consult the LM (not blank,
+    # not the repeat) the chain record and arcs of the state the frame starts in
+    lab_h, st_h = llab.cpu().numpy(), lls.cpu().numpy()
+    prev_lab = np.concatenate([np.full((Bl, 1), V, np.int32), lab_h[:, :-1]], axis=1)
+    start_st = np.concatenate([np.zeros((Bl, 1), np.int32), st_h[:, :-1]], axis=1)
+    lm_frames = (lab_h != V) & (lab_h != prev_lab)
+    lm_states = start_st[lm_frames]
+    chain_bytes = lm.query_bytes(lm_states)[0] - 8 * V * len(lm_states)
+    dec_bytes = Bl * Tl * 4 * (V + 1) + chain_bytes
+    fused_large = {"workload": f"CTC, B={Bl} utterances x {Tl} frames, {V + 1} classes, lambda={fspec.lam}, "
+                               "one launch",
+                   "ms": lm_ms, "frames_per_s": Bl * Tl / (lm_ms * 1e-3),
+                   "lm_frame_share": float(lm_frames.mean()),
+                   "algorithmic_bytes": int(dec_bytes), "algorithmic_gbps": dec_bytes / (lm_ms * 1e-3) / 1e9}
+    log(f"fused CTC decode, B={Bl} x {Tl}: {lm_ms:.2f} ms, {fused_large['frames_per_s']:.3g} frames/s, "
+        f"{fused_large['algorithmic_gbps']:.0f} GB/s algorithmic (LM on {100 * lm_frames.mean():.0f} % of frames)")
+    del lasr, llab, lls
+
     asr_host = asr_bt.contiguous().cpu().numpy() if args.cpu_seconds > 0 else None   # for the oracle's decode
     gpu_labels = labels.cpu().numpy()
     del asr, asr_bt
@@ -420,6 +465,7 @@ def main():
         "latency_b512_us": lat_us,
         "fused": fused,
         "fused_decode": fused_decode,
+        "fused_decode_large": fused_large,
         "fused_plain": fused_plain,
         "fused_topk": topk,
         "advance_graph_b512": graph,

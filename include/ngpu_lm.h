@@ -188,7 +188,9 @@ enum ngpu_fusion_mode {
  * AED (model built with NGPU_BUILD_BOS_EOS): class V is <eos>; label = argmax
  *   over v <= V of the fused score, <eos> using the state's final weight as its
  *   LM score; <eos> leaves the state unchanged, a token advances it.
- * Ties go to the lowest index.  In/out: d_states[B] (int32), d_prev[B] (CTC
+ * Ties go to the lowest index (-0 equals +0).  ASR scores may be -inf: a
+ * candidate set entirely at -inf yields its first candidate, as a strict '>'
+ * scan from index 0 does; NaN is not supported.  In/out: d_states[B] (int32), d_prev[B] (CTC
  * only; may be NULL otherwise).  Out: d_tokens[B] (int32 label, V = blank).
  * Out-of-range states give label -1, leave the state unchanged and are counted
  * for ngpu_lm_check_states.  Asynchronous on hip_stream. */
@@ -204,9 +206,12 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
  * before selection; the paper applies it to AED beam search).  Row b of the
  * outputs ([B, k] each, row-major) lists the k best in descending order of
  * the fused score, ties to the lower token index: d_tokens (int32), d_scores
- * (fp32 fused scores), d_next (int32 state after that token).  States are
- * read only.  1 <= k <= min(V, NGPU_LM_MAX_TOPK); cost grows as k * V per
- * hypothesis.  An out-of-range state gives a row of -1 tokens, NaN scores and
+ * (fp32 fused scores), d_next (int32 state after that token); when fewer
+ * than k tokens score above -inf, the rest follow in index order (as a strict
+ * '>' selection gives).  States are read only.
+ * 1 <= k <= min(V, NGPU_LM_MAX_TOPK); cost per hypothesis: one pass over the V
+ * tokens, then per selected token one wavefront reduction and a rescan of the
+ * V / 64 tokens of one lane.  An out-of-range state gives a row of -1 tokens, NaN scores and
  * -1 states and is counted for ngpu_lm_check_states.  Asynchronous. */
 int ngpu_lm_fused_topk(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t asr_ld, float lambda, int32_t k,
                        const int32_t *d_states, int32_t *d_tokens, float *d_scores, int32_t *d_next,

@@ -430,6 +430,102 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     }
 }
 
+// The same selection for V <= 256 * SPL with each lane's 4 * SPL tokens held in
+// registers (fused value and next state, bit 31 marking a token taken or past
+// V): a round's rescan and marking touch registers only.  Register arrays are
+// indexed with compile-time indices only (unrolled loops with a uniform
+// compare), so they stay in registers.
+template <int SPL>
+__global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
+                                                               int64_t ld, float lambda, int k,
+                                                               const int32_t *__restrict__ states,
+                                                               int32_t *__restrict__ tokens,
+                                                               float *__restrict__ scores,
+                                                               int32_t *__restrict__ next) {
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    if (b >= B) return;
+    const int V = t.vocab_size;
+    float *ls = lds;
+    int *ln = reinterpret_cast<int *>(ls + lds_row(V));
+    float *arow = reinterpret_cast<float *>(ln + lds_row(V));
+    int32_t *otok = tokens + b * k;
+    float *osc = scores + b * k;
+    int32_t *onx = next + b * k;
+    copy_to_lds_dword(asr + b * ld, arow, V, lane);
+    const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    if (s < 0 || s >= t.num_states) {
+        if (lane == 0) atomicAdd(&t.status[0], 1);
+        for (int j = lane; j < k; j += kWave) {
+            otok[j] = -1;
+            osc[j] = NAN;
+            onx[j] = -1;
+        }
+        wait_lds_copies();   // no copy into LDS outlives the wavefront
+        return;
+    }
+    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    constexpr int kTaken = int32_t(0x80000000u);
+    float f[SPL][4];
+    int n[SPL][4];
+    float bx = -__builtin_inff();
+    int bi = kNone;
+#pragma unroll
+    for (int c = 0; c < SPL; ++c) {
+        const int v0 = c * kStripe + 4 * lane;
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(ls + v0);
+        const i32x4 m = *reinterpret_cast<const i32x4 *>(ln + v0);
+        const f32x4 a = *reinterpret_cast<const f32x4 *>(arow + v0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float lm;
+            int nx;
+            slot_value(h, x[j], m[j], lm, nx);
+            f[c][j] = __builtin_fmaf(lambda, lm, a[j]);
+            n[c][j] = v0 + j < V ? nx : kTaken;   // padding past V counts as taken
+            if (v0 + j < V) take_max(f[c][j], v0 + j, bx, bi);
+        }
+    }
+    for (int r = 0; r < k; ++r) {
+        float wv;
+        int w = wave_argmax(bx, bi, wv);
+        if (w == kNone) {   // everything left is -inf: the lowest index not yet taken
+            int lo = kNone;
+#pragma unroll
+            for (int c = SPL - 1; c >= 0; --c)
+#pragma unroll
+                for (int j = 3; j >= 0; --j)
+                    if (n[c][j] >= 0) lo = c * kStripe + 4 * lane + j;
+            w = argmax_index(wave_max_u64(argmax_key(-__builtin_inff(), lo)));
+        }
+        const int wc = w >> 8, wj = w & 3;   // uniform: the winner's stripe and slot
+        if (lane == ((w & (kStripe - 1)) >> 2)) {   // the lane that owns token w
+            float fv = 0.0f;
+            int nv = 0;
+#pragma unroll
+            for (int c = 0; c < SPL; ++c)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (c == wc && j == wj) {
+                        fv = f[c][j];
+                        nv = n[c][j];
+                        n[c][j] |= kTaken;
+                    }
+            otok[r] = w;
+            osc[r] = fv;
+            onx[r] = nv;
+            bx = -__builtin_inff();
+            bi = kNone;
+#pragma unroll
+            for (int c = 0; c < SPL; ++c)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (n[c][j] >= 0) take_max(f[c][j], c * kStripe + 4 * lane + j, bx, bi);
+        }
+    }
+}
+
 __global__ __launch_bounds__(256) void final_weights_kernel(DevTrie t, const int32_t *__restrict__ states, int64_t B,
                                                           float *__restrict__ out) {
     const int64_t b = int64_t(blockIdx.x) * 256 + threadIdx.x;
@@ -453,8 +549,28 @@ hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int6
                              const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
                              hipStream_t stream) {
     const size_t lds = (2 * size_t(lds_row(t.vocab_size)) + size_t(asr_row_words(t.vocab_size))) * sizeof(float);
-    hipLaunchKernelGGL(fused_topk_kernel, dim3(unsigned(B)), dim3(kWave), lds, stream, t, asr, B, ld, lambda, k,
-                       states, tokens, scores, next);
+    const dim3 grid(static_cast<unsigned>(B)), block(kWave);
+    switch ((t.vocab_size + kStripe - 1) / kStripe) {   // stripes per lane
+        case 1:
+            hipLaunchKernelGGL(fused_topk_reg_kernel<1>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
+                               tokens, scores, next);
+            break;
+        case 2:
+            hipLaunchKernelGGL(fused_topk_reg_kernel<2>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
+                               tokens, scores, next);
+            break;
+        case 3:
+            hipLaunchKernelGGL(fused_topk_reg_kernel<3>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
+                               tokens, scores, next);
+            break;
+        case 4:
+            hipLaunchKernelGGL(fused_topk_reg_kernel<4>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
+                               tokens, scores, next);
+            break;
+        default:
+            hipLaunchKernelGGL(fused_topk_kernel, grid, block, lds, stream, t, asr, B, ld, lambda, k, states, tokens,
+                               scores, next);
+    }
     return hipGetLastError();
 }
 

@@ -629,6 +629,31 @@ def test_fused_topk_minus_inf_and_ties(dev, lam):
         assert ot[3, :6].tolist() == [4, 252, 256, 260, 767, 1023]
 
 
+@pytest.mark.parametrize("V", [128, 500, 700])
+def test_fused_topk_vocab_sizes(dev, V):
+    """Vocabularies of one, two and three 256-token stripes per lane (the
+    register top-k), with -inf rows and ties."""
+    m, lm, o = pair(f"topk V{V}", lambda: generate_model(V, [V, 6 * V, 6 * V], 1.0, seed=V + 7))
+    B, k = 40, 12
+    states = uniform_states(m, B, seed=V + 8)
+    asr = asr_logprobs((B, V), seed=V + 9)
+    asr[0] = -np.inf
+    asr[1] = -4.0
+    asr[2, :] = -np.inf
+    asr[2, ::37] = -1.0
+    for lam in (0.0, 0.6):
+        case(f"fused top-k V={V} k={k} lambda={lam}")
+        tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), lam, k, torch.from_numpy(states).to(dev))
+        torch.cuda.synchronize()
+        assert lm.check_states() == 0
+        ot, osc, onx = o.fused_topk(asr, lam, k, states)
+        assert np.array_equal(tok.cpu().numpy(), ot)
+        assert np.array_equal(nx.cpu().numpy(), onx)
+        g = sc.cpu().numpy()
+        fin = np.isfinite(osc)
+        assert np.array_equal(np.isfinite(g), fin) and np.abs(g[fin] - osc[fin]).max() <= TOL
+
+
 def test_fused_topk_odd_vocab_and_bad_state(dev):
     m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
     V = m.vocab_size

@@ -730,16 +730,28 @@ def test_graph_capture_replays_match_eager(dev):
     sc = torch.empty((B, V), dtype=torch.float32, device=dev)
     nx = torch.empty((B, V), dtype=torch.int32, device=dev)
     st0 = st.clone()
+    # a whole-decode launch and a top-k on their own buffers
+    dasr = torch.from_numpy(np.ascontiguousarray(asr_np.transpose(1, 0, 2))).to(dev)
+    dst = torch.empty(B, dtype=torch.int32, device=dev)
+    dprev = torch.empty(B, dtype=torch.int32, device=dev)
+    dlab = torch.empty((B, T), dtype=torch.int32, device=dev)
+    ktok = torch.empty((B, 6), dtype=torch.int32, device=dev)
+    ksc = torch.empty((B, 6), dtype=torch.float32, device=dev)
+    knx = torch.empty((B, 6), dtype=torch.int32, device=dev)
 
     def body():
         for t in range(T):
             lm.fused_greedy_step(asr[t], 0.5, st, prev, mode=ng.NGPU_FUSION_CTC, tokens=toks[t])
         lm.advance(st, sc, nx)
+        dst.copy_(st0)
+        dprev.fill_(V)
+        lm.fused_greedy_decode(dasr, 0.5, dst, dprev, mode=ng.NGPU_FUSION_CTC, labels=dlab)
+        lm.fused_topk(asr[0, :, :V], 0.7, 6, st, tokens=ktok, scores=ksc, next_states=knx)
 
     # eager reference
     body()
     torch.cuda.synchronize()
-    ref = [x.clone() for x in (toks, st, prev, sc, nx)]
+    ref = [x.clone() for x in (toks, st, prev, sc, nx, dst, dprev, dlab, ktok, ksc, knx)]
     case("graph capture of 12 fused steps and one advance")
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -760,15 +772,20 @@ def test_graph_capture_replays_match_eager(dev):
         prev.fill_(V)
         toks.fill_(-9)
         sc.fill_(float("nan"))
+        dlab.fill_(-9)
+        ktok.fill_(-9)
         g.replay()
         torch.cuda.synchronize()
-        for a, b in zip((toks, st, prev, sc, nx), ref):
+        for a, b in zip((toks, st, prev, sc, nx, dst, dprev, dlab, ktok, ksc, knx), ref):
             assert torch.equal(a, b), f"replay {r} differs"
         _ = lm.advance(st)                        # eager work between replays
         torch.cuda.synchronize()
     assert lm.check_states() == 0
     ol, os_ = o.decode(np.ascontiguousarray(asr_np.transpose(1, 0, 2)), MODE_CTC, 0.5, starts)
     assert np.array_equal(ref[0].cpu().numpy().T, ol)
+    assert np.array_equal(ref[7].cpu().numpy(), ol)           # the whole-decode launch
+    ot, _, onx = o.fused_topk(np.ascontiguousarray(asr_np[0, :, :V]), 0.7, 6, ref[1].cpu().numpy())
+    assert np.array_equal(ref[8].cpu().numpy(), ot) and np.array_equal(ref[10].cpu().numpy(), onx)
 
 
 def test_fused_zero_sizes(dev):

@@ -21,6 +21,8 @@
  *     allocates device memory and never synchronises a stream except in
  *     ngpu_lm_check_states.  Calls taking `hip_stream` enqueue work on that
  *     hipStream_t (NULL = the null stream) and return once it is enqueued.
+ *   - Queries launch on the current device, which must be the device whose
+ *     memory holds the uploaded image (NGPU_E_INVALID_ARG otherwise).
  *   - Every call returns NGPU_OK (0) or a negative NGPU_E_* code and then sets a
  *     thread-local message readable with ngpu_lm_last_error().  No call throws.
  *   - A handle may be used from several threads for queries; build, upload and

@@ -71,6 +71,17 @@ ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     return t;
 }
 
+// A query needs the uploaded image on the current device: its kernels run on
+// the current device and read the image through plain device pointers.
+int ready(const ngpu_lm *lm) {
+    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return hip_fail(hipGetLastError(), "hipGetDevice");
+    if (cur != lm->device)
+        return fail(NGPU_E_INVALID_ARG, "the trie image lives on device %d but device %d is current", lm->device, cur);
+    return NGPU_OK;
+}
+
 }  // namespace
 
 int ngpu::set_error(int code, const std::string &msg) {
@@ -146,7 +157,7 @@ int ngpu_lm_final_weights(const ngpu_lm *lm, const int32_t *d_states, int64_t B,
                           void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
     if (!lm->hdr.has_final) return fail(NGPU_E_INVALID_ARG, "the model has no </s> (build with NGPU_BUILD_BOS_EOS)");
-    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (const int rc = ready(lm)) return rc;
     if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld out of range", (long long)B);
     if (B == 0) return ok();
     if (!d_states || !d_final) return fail(NGPU_E_INVALID_ARG, "null device pointer");
@@ -180,7 +191,7 @@ int ngpu_lm_upload(ngpu_lm *lm, void *dev_buf, size_t dev_bytes, void *hip_strea
 int ngpu_lm_advance(const ngpu_lm *lm, const int32_t *d_states, int64_t B, float *d_scores, int32_t *d_next,
                     void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
-    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (const int rc = ready(lm)) return rc;
     if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld outside [0, %lld]", (long long)B,
                                             (long long)kMaxBatch);
     if (B == 0) return ok();
@@ -195,7 +206,7 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
                               float lambda, int32_t *d_states, int32_t *d_prev, int32_t *d_tokens,
                               void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
-    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (const int rc = ready(lm)) return rc;
     if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_AED)
         return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
     if (mode == NGPU_FUSION_AED && !lm->hdr.has_final)
@@ -219,7 +230,7 @@ int ngpu_lm_fused_topk(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t
                        const int32_t *d_states, int32_t *d_tokens, float *d_scores, int32_t *d_next,
                        void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
-    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (const int rc = ready(lm)) return rc;
     if (B < 0 || B > INT32_MAX) return fail(NGPU_E_INVALID_ARG, "B = %lld out of range", (long long)B);
     if (k < 1 || k > lm->V || k > NGPU_LM_MAX_TOPK)
         return fail(NGPU_E_INVALID_ARG, "k = %d outside [1, min(V, %d)]", k, NGPU_LM_MAX_TOPK);
@@ -240,7 +251,7 @@ int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B
                                 int32_t *d_states, int32_t *d_prev, int32_t *d_labels, int32_t *d_label_states,
                                 void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
-    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (const int rc = ready(lm)) return rc;
     if (mode < NGPU_FUSION_PLAIN || mode > NGPU_FUSION_AED)
         return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
     if (mode == NGPU_FUSION_AED && !lm->hdr.has_final)
@@ -266,7 +277,7 @@ int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B
 
 int ngpu_lm_check_states(const ngpu_lm *lm, void *hip_stream, int64_t *bad_count) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
-    if (!lm->dev) return fail(NGPU_E_NOT_UPLOADED, "trie not uploaded");
+    if (const int rc = ready(lm)) return rc;
     hipStream_t st = static_cast<hipStream_t>(hip_stream);
     int32_t host[4] = {0, 0, 0, 0};
     void *dstatus = static_cast<unsigned char *>(lm->dev) + lm->hdr.off_status;

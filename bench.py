@@ -51,10 +51,14 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "advance_cfg4_traffic.md")
 
 
 def kernel_source_hash() -> str:
+    """Hash of the advance kernel's sources with comments and blank lines
+    removed, so that the committed counters stay valid across comment edits."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p)) as f:
+            src = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        lines = [re.sub(r"//.*", "", ln).rstrip() for ln in src.splitlines()]
+        h.update("\n".join(ln for ln in lines if ln).encode())
     return h.hexdigest()[:16]
 
 

@@ -1,7 +1,9 @@
 // Device-side backoff walk shared by the advance and fused-step kernels.
 //
 // One wavefront (64 lanes) owns one hypothesis and a V-wide row in LDS
-// (ls[v] = score or raw dense weight, ln[v] = next state with flag bits).
+// (ls[v] = score or raw dense weight, ln[v] = next state with flag bits); the
+// fused kernels can also split a hypothesis over W wavefronts, each owning
+// every W-th stripe of 256 tokens of the row (walk_record<W>).
 // The walk of state s:
 //   1. its chain record (head + one entry per state of order >= 2 on its
 //      backoff chain) arrives in one vector load: lane 0 reads the head, lane
@@ -9,7 +11,9 @@
 //      (its order), so nothing waits on the head to fetch the levels.
 //   2. the dense row of the order-1 ancestor (which already folds in the
 //      empty context) is copied global -> LDS by the load unit into the row,
-//      together with the first stripe of sparse arcs.
+//      together with the first stripe of sparse arcs (or, when the caller
+//      already knows the dense row from the chain head, before the record
+//      load: walk_into_lds_dense_first).
 //   3. the sparse levels are applied bottom-up (order 2 first, the query
 //      state's order last), each overwriting the slots of its tokens with the
 //      final score and the next state marked kFinal, so the highest order that

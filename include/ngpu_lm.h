@@ -40,6 +40,10 @@ extern "C" {
 
 #define NGPU_LM_MAX_ORDER 10      /* the paper's models go up to order 10 */
 #define NGPU_LM_MAX_VOCAB 8192    /* a V-wide score/state row (8 bytes per token) must fit in 64 KiB of LDS */
+/* Most hypotheses (or utterances) per call: the launch grid, 64 work-items per
+ * hypothesis, must fit a 32-bit dispatch size.  Larger batches return
+ * NGPU_E_INVALID_ARG; split them into several calls. */
+#define NGPU_LM_MAX_BATCH ((int64_t)(1 << 26) - 256)
 
 enum ngpu_status {
     NGPU_OK = 0,

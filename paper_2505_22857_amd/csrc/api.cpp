@@ -46,9 +46,11 @@ int hip_fail(hipError_t e, const char *what) {
     return fail(NGPU_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// Largest batch whose grid (64 work-items per hypothesis) fits the 32-bit
-// dispatch size.
-constexpr int64_t kMaxBatch = (int64_t(1) << 26) - 256;
+// Largest batch whose grid fits the 32-bit dispatch size in work-items: 64
+// per hypothesis (256 for the four-wavefront fused kernels, used up to 512
+// hypotheses only).
+constexpr int64_t kMaxBatch = NGPU_LM_MAX_BATCH;
+static_assert(kMaxBatch * 64 <= int64_t(UINT32_MAX), "grid must fit the dispatch size");
 
 ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     const unsigned char *base = static_cast<const unsigned char *>(lm->dev);
@@ -231,7 +233,8 @@ int ngpu_lm_fused_topk(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t
                        void *hip_stream) {
     if (!lm) return fail(NGPU_E_INVALID_ARG, "null handle");
     if (const int rc = ready(lm)) return rc;
-    if (B < 0 || B > INT32_MAX) return fail(NGPU_E_INVALID_ARG, "B = %lld out of range", (long long)B);
+    if (B < 0 || B > kMaxBatch) return fail(NGPU_E_INVALID_ARG, "B = %lld outside [0, %lld]", (long long)B,
+                                            (long long)kMaxBatch);
     if (k < 1 || k > lm->V || k > NGPU_LM_MAX_TOPK)
         return fail(NGPU_E_INVALID_ARG, "k = %d outside [1, min(V, %d)]", k, NGPU_LM_MAX_TOPK);
     if (asr_ld < lm->V) return fail(NGPU_E_INVALID_ARG, "asr_ld %lld < V", (long long)asr_ld);
@@ -256,8 +259,9 @@ int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B
         return fail(NGPU_E_INVALID_ARG, "unknown fusion mode %d", mode);
     if (mode == NGPU_FUSION_AED && !lm->hdr.has_final)
         return fail(NGPU_E_INVALID_ARG, "AED fusion needs a model with </s> (NGPU_BUILD_BOS_EOS)");
-    if (B < 0 || B > INT32_MAX || T < 0) return fail(NGPU_E_INVALID_ARG, "bad sizes B=%lld T=%lld", (long long)B,
-                                                     (long long)T);
+    if (B < 0 || B > kMaxBatch || T < 0)
+        return fail(NGPU_E_INVALID_ARG, "bad sizes B=%lld (at most %lld) T=%lld", (long long)B, (long long)kMaxBatch,
+                    (long long)T);
     if (stride_b < 0 || stride_t < 0) return fail(NGPU_E_INVALID_ARG, "negative strides");
     const int64_t need = mode == NGPU_FUSION_PLAIN ? lm->V : int64_t(lm->V) + 1;
     if (T > 1 && stride_t < need) return fail(NGPU_E_INVALID_ARG, "stride_t %lld < %lld", (long long)stride_t,

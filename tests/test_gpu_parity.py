@@ -807,6 +807,24 @@ def test_fused_zero_sizes(dev):
     assert lm.check_states() == 0
 
 
+def test_batches_beyond_the_dispatch_limit_are_rejected(dev):
+    """B above NGPU_LM_MAX_BATCH (2^26 - 256) is an error for every batched call,
+    before any pointer is read."""
+    import ctypes
+    m, lm, o = cfg_pair(1)
+    big = (1 << 26) - 255
+    buf = torch.zeros(1024, dtype=torch.int32, device=dev)
+    p = ctypes.c_void_p(buf.data_ptr())
+    L, h = lm._lib, lm._h
+    case("batches beyond the dispatch limit")
+    assert L.ngpu_lm_advance(h, p, big, p, p, None) == -1
+    assert L.ngpu_lm_fused_greedy_step(h, p, big, m.vocab_size + 1, 1, ctypes.c_float(0.5), p, p, p, None) == -1
+    assert L.ngpu_lm_fused_topk(h, p, big, m.vocab_size, ctypes.c_float(0.5), 3, p, p, p, p, None) == -1
+    assert L.ngpu_lm_fused_greedy_decode(h, p, big, 1, m.vocab_size + 1, m.vocab_size + 1, None, 1,
+                                         ctypes.c_float(0.5), p, p, p, None, None) == -1
+    assert L.ngpu_lm_final_weights(h, p, big, p, None) in (-1,)   # no </s>: rejected either way
+
+
 def test_fused_out_of_range_state(dev):
     m, lm, o = cfg_pair(1)
     V = m.vocab_size

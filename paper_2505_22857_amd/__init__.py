@@ -23,6 +23,7 @@ NGPU_BUILD_BOS_EOS = 1
 NGPU_BUILD_REPAIR_CLOSURE = 2
 MAX_ORDER = 10
 MAX_VOCAB = 8192
+MAX_BATCH = (1 << 26) - 256      # NGPU_LM_MAX_BATCH
 
 ERROR_NAMES = {
     -1: "INVALID_ARG", -2: "TOKEN_RANGE", -3: "ORDER_RANGE", -4: "DUPLICATE_NGRAM",

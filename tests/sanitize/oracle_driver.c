@@ -28,6 +28,10 @@ int oracle_decode(const oracle_model *m, const float *asr, int64_t B, int64_t T,
 int oracle_fused_topk(const oracle_model *m, const float *asr, int64_t B, int64_t ld, float lambda, int k,
                       const int32_t *states, int32_t *tokens, float *scores, int32_t *next);
 int oracle_final(const oracle_model *m, const int32_t *states, int64_t B, float *out);
+int oracle_repair(int32_t V, int32_t N, int64_t M, const int32_t *order, const int32_t *tokens,
+                  const float *logprob, const float *backoff, float unk_logprob, int flags, int64_t *M_out,
+                  int32_t **order_out, int32_t **tokens_out, float **W_out, float **B_out);
+void oracle_free_buffer(void *p);
 
 static void *read_all(const char *path, size_t *n) {
     FILE *f = fopen(path, "rb");
@@ -43,8 +47,40 @@ static void *read_all(const char *path, size_t *n) {
 
 static void put(FILE *f, const void *p, size_t bytes) { fwrite(p, 1, bytes, f); }
 
+/* oracle_driver repair LIST OUT: the repaired list (int64 M, then order, tokens, W, B). */
+static int repair_main(const char *list_path, const char *out_path) {
+    size_t n = 0;
+    char *buf = (char *)read_all(list_path, &n);
+    if (!buf || n < 24) return 2;
+    int32_t V = *(int32_t *)buf, N = *(int32_t *)(buf + 4);
+    int64_t M = *(int64_t *)(buf + 8);
+    float unk = *(float *)(buf + 16);
+    uint32_t flags = *(uint32_t *)(buf + 20);
+    const int32_t *order = (const int32_t *)(buf + 24);
+    const int32_t *tokens = order + M;
+    const float *W = (const float *)(tokens + M * N);
+    const float *Bk = W + M;
+    int64_t M2 = 0;
+    int32_t *o2 = NULL, *t2 = NULL;
+    float *w2 = NULL, *b2 = NULL;
+    int rc = oracle_repair(V, N, M, order, tokens, W, Bk, unk, (int)(flags & 1u), &M2, &o2, &t2, &w2, &b2);
+    if (rc) { fprintf(stderr, "oracle_repair rc %d\n", rc); free(buf); return 3; }
+    FILE *out = fopen(out_path, "wb");
+    put(out, &M2, sizeof M2);
+    put(out, o2, sizeof(int32_t) * (size_t)M2);
+    put(out, t2, sizeof(int32_t) * (size_t)(M2 * N));
+    put(out, w2, sizeof(float) * (size_t)M2);
+    put(out, b2, sizeof(float) * (size_t)M2);
+    fclose(out);
+    oracle_free_buffer(o2); oracle_free_buffer(t2); oracle_free_buffer(w2); oracle_free_buffer(b2);
+    free(buf);
+    printf("rc 0 rows %lld\n", (long long)M2);
+    return 0;
+}
+
 int main(int argc, char **argv) {
-    if (argc != 5) { fprintf(stderr, "usage: oracle_driver LIST ASR K OUT\n"); return 2; }
+    if (argc == 4 && argv[1][0] == 'r') return repair_main(argv[2], argv[3]);
+    if (argc != 5) { fprintf(stderr, "usage: oracle_driver LIST ASR K OUT | repair LIST OUT\n"); return 2; }
     size_t n = 0, na = 0;
     char *buf = (char *)read_all(argv[1], &n);
     char *abuf = (char *)read_all(argv[2], &na);

@@ -106,6 +106,20 @@ def test_builder_repair_clean_and_identical(drivers, seed):
     assert np.array_equal(np.fromfile(img, np.uint8), ref)
 
 
+@pytest.mark.parametrize("seed", [6, 7])
+def test_oracle_repair_clean_and_identical(drivers, seed):
+    _, od, d = drivers
+    m = generate_model(8, [8, 40, 90, 100], 1.0, seed=seed)
+    o, t, W, B = pruned_list(m, 0.35, seed=seed + 100)
+    lst, out = str(d / f"orep{seed}.list"), str(d / f"orep{seed}.out")
+    _write_list(lst, 8, 4, o, t, W, B, m.unk_logprob, 0)
+    _run([od, "repair", lst, out])
+    ro, rt, rW, rB = oracle.repair_list(8, 4, o, t, W, B, m.unk_logprob)
+    want = (np.array([len(ro)], np.int64).tobytes() + ro.astype(np.int32).tobytes() + rt.astype(np.int32).tobytes()
+            + rW.astype(np.float32).tobytes() + rB.astype(np.float32).tobytes())
+    assert open(out, "rb").read() == want
+
+
 def _broken_lists():
     m = tiny_model(9, 3, seed=21, n_unigrams=9)
     o, t, W, B = m.to_list()

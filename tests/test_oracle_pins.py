@@ -379,6 +379,25 @@ def test_ctc_lambda_zero_is_textbook_greedy_ctc(oracle_lib):
         assert adv == collapse(raw[b])
 
 
+def test_transducer_lambda_zero_is_raw_argmax(oracle_lib):
+    """At lambda = 0 the transducer rule is the raw argmax over V + 1 classes
+    (blank kept), and the state follows the emitted tokens."""
+    model = make_config_model(1)
+    o = Oracle.from_model(model)
+    V = model.vocab_size
+    asr = asr_logprobs((6, 40, V + 1), seed=71, blank_boost=2.0)
+    asr[0, 3, :] = -2.0                         # a full tie: index 0
+    labels, states = o.decode(asr, MODE_TRANSDUCER, 0.0)
+    assert np.array_equal(labels, np.argmax(asr, axis=-1))
+    for b in range(asr.shape[0]):
+        st = 0
+        for t in range(asr.shape[1]):
+            if labels[b, t] != V:
+                _, nx, _ = o.advance(np.array([st], np.int32))
+                st = int(nx[0, labels[b, t]])
+            assert states[b, t] == st
+
+
 def test_topk_reductions(oracle_lib):
     """k = 1 is the plain greedy step; lambda = 0 is a stable descending sort of the ASR row;
     k = V lists every token once, fused scores non-increasing."""

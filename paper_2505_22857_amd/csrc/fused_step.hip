@@ -255,7 +255,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
 // Whole greedy decode: utterance b runs frames 0 .. len_b - 1 of
 // asr[b * stride_b + t * stride_t + class]; one utterance per workgroup of W
 // wavefronts.
-template <int MODE, int W>
+template <int MODE, int W, int NB>
 __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                                   int64_t T, int64_t stride_b, int64_t stride_t,
                                                                   const int32_t *__restrict__ lengths, float lambda,
@@ -270,10 +270,15 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
     if (b >= B) return;
     const int V = t.vocab_size;
     const int rowp = asr_row_words(V);
+    // ASR rows: NB = 2 buffers, the next row's copy riding along with the walk
+    // (while every utterance is resident at once, the latency-bound case), or
+    // NB = 1 buffer, refilled once the frame has read it (when more utterances
+    // than fit wait for a CU: the smaller LDS footprint lets more run at once)
+    constexpr int kRowBufs = NB;
     float *ls = lds;
     int *ln = reinterpret_cast<int *>(ls + lds_row(V));
-    float *abuf = reinterpret_cast<float *>(ln + lds_row(V));   // two ASR rows, double-buffered
-    Exchange *xc = reinterpret_cast<Exchange *>(abuf + 2 * rowp);
+    float *abuf = reinterpret_cast<float *>(ln + lds_row(V));
+    Exchange *xc = reinterpret_cast<Exchange *>(abuf + kRowBufs * rowp);
     int32_t *lab = labels + b * T;
     int32_t *lst = label_states ? label_states + b * T : nullptr;
 
@@ -302,13 +307,16 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
         // frame f reads its ASR row from LDS, copied during frame f - 1 (or
         // before the loop); the walk also starts the copy of row f + 1
         wait_lds_copies();
-        float *cur = abuf + (f & 1) * rowp;
-        float *nxt = abuf + ((f + 1) & 1) * rowp;
+        float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
+        float *nxt = abuf + (kRowBufs == 2 ? ((f + 1) & 1) * rowp : 0);
         const bool more = f + 1 < len;
         const float *pf = more ? row + stride_t : nullptr;
         const float next_v = (MODE != kPlain && more) ? row[stride_t + V] : 0.0f;
-        const int label = greedy_step<MODE, W, false>(t, cur, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, pf,
-                                                      nxt, V);
+        const int label = greedy_step<MODE, W, false>(t, cur, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane,
+                                                      kRowBufs == 2 ? pf : nullptr, nxt, V);
+        // one buffer: every read of this frame's row has completed (its values
+        // were consumed by the argmax), so the next row can be copied over it
+        if (kRowBufs == 1 && pf) copy_stripes_dword<W>(pf, cur, V, wave, lane);
         rowV = next_v;
         if (MODE == kCtc) pv = label;
         // Lane f % 64 of wavefront 0 keeps frame f's label and state; one
@@ -607,28 +615,43 @@ hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int6
     }
 }
 
-template <int MODE, int W>
+template <int MODE, int W, int NB>
 static hipError_t launch_decode_w(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
                                   const int32_t *lengths, float lambda, int32_t *states, int32_t *prev,
                                   int32_t *labels, int32_t *label_states, hipStream_t stream) {
-    hipLaunchKernelGGL((fused_decode_kernel<MODE, W>), dim3(unsigned(B)), dim3(W * kWave),
-                       hyp_lds_bytes(t.vocab_size, 2), stream, t, asr, B, T, sb, st, lengths, lambda, states, prev,
+    hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB>), dim3(unsigned(B)), dim3(W * kWave),
+                       hyp_lds_bytes(t.vocab_size, NB), stream, t, asr, B, T, sb, st, lengths, lambda, states, prev,
                        labels, label_states);
     return hipGetLastError();
+}
+
+// Utterances the device holds at once with two ASR row buffers per utterance
+// (one wavefront each): CUs times the workgroups whose LDS fits one CU.
+static int64_t resident_double_buffered(const DevTrie &t) {
+    int dev = 0, cus = 0, lds = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return INT64_MAX;   // unknown: keep two buffers
+    }
+    return int64_t(cus) * int64_t(size_t(lds) / hyp_lds_bytes(t.vocab_size, 2));
 }
 
 template <int MODE>
 static hipError_t launch_decode_mode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb,
                                      int64_t st, const int32_t *lengths, float lambda, int32_t *states,
                                      int32_t *prev, int32_t *labels, int32_t *label_states, hipStream_t stream) {
-    switch (waves_per_hyp(B)) {
-        case 4:
-            return launch_decode_w<MODE, 4>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
-                                            label_states, stream);
-        default:
-            return launch_decode_w<MODE, 1>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
-                                            label_states, stream);
-    }
+    if (waves_per_hyp(B) == 4)
+        return launch_decode_w<MODE, 4, 2>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
+                                           stream);
+    // measured on the 20M 6-gram (two buffers hold 2304 utterances on 256 CUs):
+    // one buffer is 5 % slower at B = 1024-2048 and 9-13 % faster at 4096-8192
+    if (B <= resident_double_buffered(t))
+        return launch_decode_w<MODE, 1, 2>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
+                                           stream);
+    return launch_decode_w<MODE, 1, 1>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
+                                       stream);
 }
 
 hipError_t launch_fused_decode(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,

@@ -397,10 +397,11 @@ def test_decode_launch_modes_ragged_lengths(dev, mode):
     assert np.array_equal(fin, os_[:, -1])
 
 
-@pytest.mark.parametrize("B", [513, 1100])
+@pytest.mark.parametrize("B", [513, 1100, 5000])
 def test_fused_larger_batches(dev, B):
     """Batches above 512 hypotheses, which run with one wavefront per hypothesis
-    instead of four."""
+    instead of four; at 5000 utterances (more than the 256 CUs hold at once
+    with two V = 1024 ASR rows each) the whole decode keeps one row buffer."""
     m, lm, o = cfg_pair(2)
     V = m.vocab_size
     T = 16

@@ -29,6 +29,10 @@ namespace ngpu {
 
 enum { kPlain = 0, kCtc = 1, kTransducer = 2, kAed = 3 };
 
+// Word 3 of a raw (unformatted, unswizzled) buffer resource on gfx9-family
+// chips: 32-bit data format; reads past the resource's byte range return 0.
+constexpr int kBufferConfig = 0x00020000;
+
 // Words of an ASR row buffer in LDS: the V tokens rounded up to whole
 // stripes, so that the 16-byte reads of the scans stay inside it.  (Blank or
 // <eos>, class V, travels in a register.)
@@ -80,6 +84,83 @@ __device__ __forceinline__ void scan_fused(const ChainHead &h, const float *ls, 
     for (int c = kStripe * wave; c < full; c += kStripe * W) four(c + 4 * lane, false);
     if (full < V && owns_token<W>(full, wave)) four(full + 4 * lane, true);
 }
+
+// ASR row held in LDS (asr_row_words(V) words; the owned stripes are read).
+template <int W>
+struct LdsAsr {
+    const float *row;
+    __device__ __forceinline__ void argmax(int V, int wave, int lane, float &bx, int &bi) const {
+        scan_row<W>(row, V, wave, lane, bx, bi);
+    }
+    template <int MODE>
+    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln, float lambda, int pv,
+                                          int V, int wave, int lane, float &bx, int &bi) const {
+        scan_fused<MODE, W>(h, ls, ln, row, lambda, pv, V, wave, lane, bx, bi);
+    }
+};
+
+// ASR row held in registers, for V <= kRegTokens: lane l of wavefront w keeps
+// classes 256 c + 64 j + l (j = 0 .. 3) of each owned stripe c, in ascending
+// order, so each of its loads is one coalesced 256-byte read and the scans
+// read the walked LDS row one word per lane (no bank conflicts).  The row is
+// read through a buffer resource of V words: classes past V read as 0 without
+// a branch (the scans skip them), so the loads are straight-line code and the
+// compiler's waits for the chain record issued just before them can leave
+// them in flight.  FULL: V = kRegTokens, every class present and nothing to
+// skip (the per-class conditions would otherwise be held across the frame
+// loop in scalar registers).
+constexpr int kRegTokens = 1024;
+
+template <int W, bool FULL>
+struct RegAsr {
+    static constexpr int kN = kRegTokens / (kWave * W);   // values per lane
+    float a[kN];
+
+    // first class of value i of this wavefront (uniform); the lane adds its index
+    __device__ static __forceinline__ int base(int i, int wave) {
+        return kStripe * (W * (i / 4) + (W == 1 ? 0 : wave)) + kWave * (i % 4);
+    }
+
+    // (the resource starts at this wavefront's first stripe: the range check
+    // covers the lane and instruction offsets, not a scalar offset)
+    __device__ __forceinline__ void load(const float *row, int V, int wave, int lane) {
+        const int w0 = W == 1 ? 0 : kStripe * wave;
+        const int n = V > w0 ? V - w0 : 0;
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(row + w0), short(0),
+                                                                           n * int(sizeof(float)), kBufferConfig);
+#pragma unroll
+        for (int i = 0; i < kN; ++i)
+            a[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                 r, (kStripe * W * (i / 4) + kWave * (i % 4) + lane) * int(sizeof(float)),
+                                                 0, 0));
+    }
+    __device__ __forceinline__ void argmax(int V, int wave, int lane, float &bx, int &bi) const {
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+            const int v = base(i, wave) + lane;
+            if (FULL || base(i, wave) + kWave <= V || v < V) take_max(a[i], v, bx, bi);
+        }
+    }
+    template <int MODE>
+    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln, float lambda, int pv,
+                                          int V, int wave, int lane, float &bx, int &bi) const {
+#pragma unroll
+        for (int i = 0; i < kN; ++i) {
+            const int b0 = base(i, wave);
+            if (!FULL && b0 >= V) continue;   // uniform; the slots read below lie inside the padded row
+            const int v = b0 + lane;
+            float lm;
+            int nx;
+            slot_value(h, ls[v], ln[v], lm, nx);
+            const float f = __builtin_fmaf(lambda, lm, a[i]);
+            if ((MODE != kCtc || v != pv) && (FULL || b0 + kWave <= V || v < V)) take_max(f, v, bx, bi);
+        }
+    }
+};
+
+struct NoHook {
+    __device__ __forceinline__ void operator()() const {}
+};
 
 // Exchange area of W wavefronts: two alternating buffers of W (key, payload)
 // pairs, so one barrier per exchange suffices (a buffer is written again only
@@ -153,27 +234,30 @@ __device__ __forceinline__ int first_token_state(const ChainHead &h, const float
     return ns;
 }
 
-// One fused greedy step of a hypothesis held by W wavefronts.  row: its V
-// token ASR log-probabilities in LDS (asr_row_words(V) words, owned stripes
-// landed unless ROW_PENDING, in which case their copy was issued just before);
+// One fused greedy step of a hypothesis held by W wavefronts.  asr: its V
+// token ASR log-probabilities (LdsAsr: owned stripes landed unless
+// ROW_PENDING, in which case their copy was issued just before; RegAsr);
 // rowV: class V (blank, or <eos> in AED mode).  s: valid state (uniform); pv:
-// previous label (CTC).  Returns the label and updates s; all lanes of all W
-// wavefronts return the same values.
-template <int MODE, int W, bool ROW_PENDING>
-__device__ __forceinline__ int greedy_step(const DevTrie &t, const float *row, float rowV, float lambda, int &s,
+// previous label (CTC).  after_record runs once the chain record's load is
+// issued.  Returns the label and updates s; all lanes of all W wavefronts
+// return the same values.
+template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook>
+__device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, float rowV, float lambda, int &s,
                                            int pv, float *ls, int *ln, Exchange *xc, int &xi, int wave, int lane,
-                                           const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0) {
+                                           const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0,
+                                           AfterRecord after_record = {}) {
     const int V = t.vocab_size;
     const float fin = MODE == kAed ? t.final_w[s] : 0.0f;   // <eos> takes the state's final weight
     // The chain record is fetched first: in CTC and transducer modes its load
     // overlaps the plain ASR argmax, which may still find that the LM is not needed.
     int nlev;
     const int4 rec = fetch_record(t, s, lane, nlev);
+    after_record();
     if (MODE == kCtc || MODE == kTransducer) {
         if (ROW_PENDING) wait_lds_copies();
         float bx = -__builtin_inff(), av;
         int bi = kNone, unused;
-        scan_row<W>(row, V, wave, lane, bx, bi);
+        asr.argmax(V, wave, lane, bx, bi);
         int a = group_argmax<W>(bx, bi, 0, av, unused, xc, xi, wave, lane);
         if (a == kNone) a = 0;                    // every token at -inf: the first one, unless blank beats it
         if (rowV > av) a = V;                     // blank only when strictly larger (it has the highest index)
@@ -185,7 +269,7 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const float *row, f
     const ChainHead h = walk_record<W>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
     float bx = -__builtin_inff(), wv;
     int bi = kNone;
-    scan_fused<MODE, W>(h, ls, ln, row, lambda, pv, V, wave, lane, bx, bi);
+    asr.template fused<MODE>(h, ls, ln, lambda, pv, V, wave, lane, bx, bi);
     // each lane's candidate next state rides along with its key (read from its own stripe)
     int cand = 0;
     if (bi != kNone) {
@@ -244,7 +328,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     int xi = 0;
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
-    const int label = greedy_step<MODE, W, true>(t, arow, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
+    const int label = greedy_step<MODE, W, true>(t, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
     if (wave == 0 && lane == 0) {
         tokens[b] = label;
         states[b] = s;
@@ -254,8 +338,9 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
 
 // Whole greedy decode: utterance b runs frames 0 .. len_b - 1 of
 // asr[b * stride_b + t * stride_t + class]; one utterance per workgroup of W
-// wavefronts.
-template <int MODE, int W, int NB>
+// wavefronts.  NB: ASR row buffers in LDS (1 or 2), or 0 for rows held in
+// registers (V <= kRegTokens; FULL: V = kRegTokens).
+template <int MODE, int W, int NB, bool FULL = false>
 __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                                   int64_t T, int64_t stride_b, int64_t stride_t,
                                                                   const int32_t *__restrict__ lengths, float lambda,
@@ -273,8 +358,10 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
     // ASR rows: NB = 2 buffers, the next row's copy riding along with the walk
     // (while every utterance is resident at once, the latency-bound case), or
     // NB = 1 buffer, refilled once the frame has read it (when more utterances
-    // than fit wait for a CU: the smaller LDS footprint lets more run at once)
+    // than fit wait for a CU: the smaller LDS footprint lets more run at once),
+    // or in registers (NB = 0), the next row loaded behind the chain record
     constexpr int kRowBufs = NB;
+    RegAsr<W, FULL> cur_r;
     float *ls = lds;
     int *ln = reinterpret_cast<int *>(ls + lds_row(V));
     float *abuf = reinterpret_cast<float *>(ln + lds_row(V));
@@ -300,23 +387,41 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
     }
     int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
     const float *row = asr + b * stride_b;
-    if (len > 0) copy_stripes_dword<W>(row, abuf, V, wave, lane);
+    if (len > 0) {
+        if (kRowBufs == 0)
+            cur_r.load(row, V, wave, lane);
+        else
+            copy_stripes_dword<W>(row, abuf, V, wave, lane);
+    }
     float rowV = (MODE != kPlain && len > 0) ? row[V] : 0.0f;
     int keep_lab = -1, keep_st = -1, xi = 0;
     for (int64_t f = 0; f < len; ++f, row += stride_t) {
-        // frame f reads its ASR row from LDS, copied during frame f - 1 (or
-        // before the loop); the walk also starts the copy of row f + 1
-        wait_lds_copies();
-        float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
-        float *nxt = abuf + (kRowBufs == 2 ? ((f + 1) & 1) * rowp : 0);
+        // LDS rows: frame f reads its ASR row from LDS, copied during frame
+        // f - 1 (or before the loop); the walk also starts the copy of row
+        // f + 1.  (The wait comes before any load of this frame is issued.)
+        if (kRowBufs > 0) wait_lds_copies();
         const bool more = f + 1 < len;
         const float *pf = more ? row + stride_t : nullptr;
         const float next_v = (MODE != kPlain && more) ? row[stride_t + V] : 0.0f;
-        const int label = greedy_step<MODE, W, false>(t, cur, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane,
-                                                      kRowBufs == 2 ? pf : nullptr, nxt, V);
-        // one buffer: every read of this frame's row has completed (its values
-        // were consumed by the argmax), so the next row can be copied over it
-        if (kRowBufs == 1 && pf) copy_stripes_dword<W>(pf, cur, V, wave, lane);
+        int label;
+        if constexpr (kRowBufs == 0) {
+            // the last frame reloads its own row: with no branch around the
+            // loads the compiler's count of loads in flight stays exact
+            RegAsr<W, FULL> nxt_r;
+            const float *src = more ? pf : row;
+            auto load_next = [&]() { nxt_r.load(src, V, wave, lane); };
+            label = greedy_step<MODE, W, false>(t, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr,
+                                                nullptr, 0, load_next);
+            cur_r = nxt_r;
+        } else {
+            float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
+            float *nxt = abuf + (kRowBufs == 2 ? ((f + 1) & 1) * rowp : 0);
+            label = greedy_step<MODE, W, false>(t, LdsAsr<W>{cur}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane,
+                                                kRowBufs == 2 ? pf : nullptr, nxt, V);
+            // one buffer: every read of this frame's row has completed (its values
+            // were consumed by the argmax), so the next row can be copied over it
+            if (kRowBufs == 1 && pf) copy_stripes_dword<W>(pf, cur, V, wave, lane);
+        }
         rowV = next_v;
         if (MODE == kCtc) pv = label;
         // Lane f % 64 of wavefront 0 keeps frame f's label and state; one
@@ -615,11 +720,11 @@ hipError_t launch_fused_step(const DevTrie &t, const float *asr, int64_t B, int6
     }
 }
 
-template <int MODE, int W, int NB>
+template <int MODE, int W, int NB, bool FULL = false>
 static hipError_t launch_decode_w(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
                                   const int32_t *lengths, float lambda, int32_t *states, int32_t *prev,
                                   int32_t *labels, int32_t *label_states, hipStream_t stream) {
-    hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB>), dim3(unsigned(B)), dim3(W * kWave),
+    hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB, FULL>), dim3(unsigned(B)), dim3(W * kWave),
                        hyp_lds_bytes(t.vocab_size, NB), stream, t, asr, B, T, sb, st, lengths, lambda, states, prev,
                        labels, label_states);
     return hipGetLastError();
@@ -645,10 +750,20 @@ static hipError_t launch_decode_mode(const DevTrie &t, const float *asr, int64_t
     if (waves_per_hyp(B) == 4)
         return launch_decode_w<MODE, 4, 2>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
                                            stream);
-    // measured on the 20M 6-gram (two buffers hold 2304 utterances on 256 CUs):
-    // one buffer is 5 % slower at B = 1024-2048 and 9-13 % faster at 4096-8192
+    // Measured on the 20M 6-gram, CTC, 200 frames: while every utterance is
+    // resident with two LDS row buffers (2304 utterances on 256 CUs at
+    // V = 1024), those are 2-4 % faster than rows in registers; beyond that
+    // the register rows (up to 16 utterances per CU) are 27 % faster at 4096
+    // utterances and 18 % at 8192, and one LDS buffer (13 per CU) still beats
+    // two by 8-14 %.
     if (B <= resident_double_buffered(t))
         return launch_decode_w<MODE, 1, 2>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
+                                           stream);
+    if (t.vocab_size == kRegTokens)
+        return launch_decode_w<MODE, 1, 0, true>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels,
+                                                 label_states, stream);
+    if (t.vocab_size < kRegTokens)
+        return launch_decode_w<MODE, 1, 0>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
                                            stream);
     return launch_decode_w<MODE, 1, 1>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
                                        stream);

@@ -401,7 +401,8 @@ def test_decode_launch_modes_ragged_lengths(dev, mode):
 def test_fused_larger_batches(dev, B):
     """Batches above 512 hypotheses, which run with one wavefront per hypothesis
     instead of four; at 5000 utterances (more than the 256 CUs hold at once
-    with two V = 1024 ASR rows each) the whole decode keeps one row buffer."""
+    with two V = 1024 ASR rows in LDS each) the whole decode keeps the rows in
+    registers."""
     m, lm, o = cfg_pair(2)
     V = m.vocab_size
     T = 16
@@ -415,6 +416,32 @@ def test_fused_larger_batches(dev, B):
         gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev, lengths=lengths)
         ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS, lengths=lengths)
         assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+
+
+@pytest.mark.parametrize("V,B", [(1000, 2400), (1024, 2400), (1025, 600), (1025, 2000), (2048, 1000), (2048, 1500)])
+def test_decode_launch_row_placements(dev, V, B):
+    """The whole decode with one wavefront per utterance keeps the ASR rows in
+    two LDS buffers while every utterance is resident at once with them (on
+    256 CUs with 160 KiB of LDS each: 2304 utterances at V <= 1024, 1792 at
+    V = 1025, 1024 at V = 2048); beyond that in registers up to V = 1024 (with
+    and without a last register chunk cut short by V), else in one LDS buffer.
+    The cases cover each placement, and the four fusion modes on the register
+    paths."""
+    m, lm, o = pair(f"V{V}", lambda: generate_model(V, [V, 20000, 15000], 1.0, seed=V, bos_eos=True))
+    T = 10
+    starts = uniform_states(m, B, seed=B + 3)
+    asr = asr_logprobs((B, T, V + 1), seed=B + 4, blank_boost=1.0)
+    lengths = np.random.default_rng(B + 5).integers(0, T + 1, B).astype(np.int32)
+    modes = (MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER, MODE_AED) if V <= 1024 else (MODE_PLAIN, MODE_CTC)
+    for mode in modes:
+        a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+        case(f"decode launch V={V} B={B} mode={mode} ragged")
+        gl, gs, fin, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev, lengths=lengths)
+        assert lm.check_states() == 0
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS, lengths=lengths)
+        bad = np.argwhere(gl != ol)
+        assert len(bad) == 0, f"labels differ first at {bad[0]}"
+        assert np.array_equal(gs, os_)
 
 
 def test_decode_launch_resumes_exactly(dev):

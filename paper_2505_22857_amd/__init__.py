@@ -234,6 +234,10 @@ class NgpuLM:
                                          _stream_handle(stream)))
         return scores, next_states
 
+    def _classes(self, mode: int) -> int:
+        """Classes an ASR row holds in ``mode``: V, plus blank (or <eos>) outside plain fusion."""
+        return self.vocab_size + (0 if mode == NGPU_FUSION_PLAIN else 1)
+
     def fused_greedy_step(self, asr, lam: float, states, prev=None, mode: int = NGPU_FUSION_PLAIN,
                           tokens=None, stream=None):
         """One greedy fusion step; ``states`` (and ``prev`` for CTC) are updated in place."""
@@ -241,6 +245,8 @@ class NgpuLM:
         if asr.dim() != 2 or asr.stride(1) != 1:
             raise TypeError("asr must be a [B, ld] tensor with unit stride in the last dimension")
         B = asr.shape[0]
+        if asr.shape[1] < self._classes(mode):
+            raise ValueError(f"asr rows must hold {self._classes(mode)} classes for mode {mode}")
         if states.numel() != B or (prev is not None and prev.numel() != B):
             raise ValueError("states/prev must hold B entries")
         if tokens is None:
@@ -271,6 +277,8 @@ class NgpuLM:
         if asr.dim() != 2 or asr.stride(1) != 1 or asr.dtype != torch.float32 or not asr.is_cuda:
             raise TypeError("asr must be a float32 [B, ld] device tensor with unit stride in the last dimension")
         B = asr.shape[0]
+        if asr.shape[1] < self.vocab_size:
+            raise ValueError(f"asr rows must hold {self.vocab_size} classes")
         if states.numel() != B:
             raise ValueError("states must hold B entries")
         tok = torch.empty((B, k), dtype=torch.int32, device=asr.device) if tokens is None else tokens
@@ -293,7 +301,9 @@ class NgpuLM:
         import torch
         if asr.dim() != 3 or asr.stride(2) != 1 or asr.dtype != torch.float32 or not asr.is_cuda:
             raise TypeError("asr must be a float32 [B, T, C] device tensor with unit class stride")
-        B, T, _ = asr.shape
+        B, T, C = asr.shape
+        if C < self._classes(mode):
+            raise ValueError(f"asr rows must hold {self._classes(mode)} classes for mode {mode}")
         if states.numel() != B or (prev is not None and prev.numel() != B):
             raise ValueError("states/prev must hold B entries")
         if labels is None:

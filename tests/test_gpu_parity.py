@@ -444,6 +444,38 @@ def test_decode_launch_row_placements(dev, V, B):
         assert np.array_equal(gs, os_)
 
 
+@pytest.mark.parametrize("V,B", [(1024, 32), (1024, 600), (1024, 2400), (1000, 2400)])
+def test_decode_launch_time_major_view(dev, V, B):
+    """The whole decode reads a time-major [T, B, C] buffer through a permuted
+    [B, T, C] view (utterance stride C, frame stride B * C) whose rows carry
+    padding past the classes: every row placement (four wavefronts, two LDS
+    buffers, registers with and without a short last chunk) must read only
+    the V (+ 1) classes of its own row."""
+    if V == 1024:
+        m, lm, o = cfg_pair(2)
+    else:
+        m, lm, o = pair(f"V{V}", lambda: generate_model(V, [V, 20000, 15000], 1.0, seed=V, bos_eos=True))
+    T, pad = 9, 7
+    starts = uniform_states(m, B, seed=B + 6)
+    asr = asr_logprobs((B, T, V + 1), seed=B + 7, blank_boost=1.0)
+    for mode in (MODE_PLAIN, MODE_CTC):
+        C = V if mode == MODE_PLAIN else V + 1
+        a = np.ascontiguousarray(asr[:, :, :C])
+        tm = np.full((T, B, C + pad), 7.0, np.float32)     # padding above every log-probability
+        tm[:, :, :C] = a.transpose(1, 0, 2)
+        view = torch.from_numpy(tm).to(dev).permute(1, 0, 2)[:, :, :C]
+        assert view.stride() == (C + pad, B * (C + pad), 1)
+        st = torch.from_numpy(starts.copy()).to(dev)
+        prev = torch.full((B,), V, dtype=torch.int32, device=dev) if mode == MODE_CTC else None
+        case(f"decode launch time-major view V={V} B={B} mode={mode}")
+        lab = lm.fused_greedy_decode(view, 0.5, st, prev, mode=mode)
+        torch.cuda.synchronize()
+        assert lm.check_states() == 0
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
+        assert np.array_equal(lab.cpu().numpy(), ol)
+        assert np.array_equal(st.cpu().numpy(), os_[:, -1])
+
+
 def test_decode_launch_resumes_exactly(dev):
     """Two launches over frames [0, 40) and [40, 90), passing states and labels
     back, equal one decode over all 90 frames."""
@@ -851,6 +883,29 @@ def test_batches_beyond_the_dispatch_limit_are_rejected(dev):
     assert L.ngpu_lm_fused_greedy_decode(h, p, big, 1, m.vocab_size + 1, m.vocab_size + 1, None, 1,
                                          ctypes.c_float(0.5), p, p, p, None, None) == -1
     assert L.ngpu_lm_final_weights(h, p, big, p, None) in (-1,)   # no </s>: rejected either way
+
+
+def test_binding_rejects_short_asr_rows(dev):
+    """The binding checks the class width the C-ABI cannot see: V classes, plus
+    blank (or <eos>) outside plain fusion."""
+    m, lm, o = cfg_pair(1)
+    V = m.vocab_size
+    st = torch.zeros(4, dtype=torch.int32, device=dev)
+    prev = torch.full((4,), V, dtype=torch.int32, device=dev)
+    case("binding: short asr rows")
+    with pytest.raises(ValueError):
+        lm.fused_greedy_step(torch.zeros((4, V), device=dev), 0.5, st, prev, mode=ng.NGPU_FUSION_CTC)
+    with pytest.raises(ValueError):
+        lm.fused_greedy_decode(torch.zeros((4, 3, V), device=dev), 0.5, st, prev, mode=ng.NGPU_FUSION_CTC)
+    with pytest.raises(ValueError):
+        lm.fused_greedy_decode(torch.zeros((4, 3, V + 1), device=dev)[:, :, :V - 1], 0.5, st)
+    with pytest.raises(ValueError):
+        lm.fused_topk(torch.zeros((4, V - 1), device=dev), 0.5, 2, st)
+    # plain fusion takes V classes; wider rows are fine
+    lm.fused_greedy_step(torch.zeros((4, V), device=dev), 0.5, st)
+    lm.fused_greedy_decode(torch.zeros((4, 3, V + 9), device=dev), 0.5, st, prev, mode=ng.NGPU_FUSION_CTC)
+    torch.cuda.synchronize()
+    assert lm.check_states() == 0
 
 
 def test_fused_out_of_range_state(dev):

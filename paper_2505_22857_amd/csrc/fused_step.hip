@@ -10,9 +10,10 @@
 // with no HBM write of the row), merges the dense row of the order-1 ancestor,
 // forms fmaf(lambda, lm[v], asr[v]) per token and takes the argmax with
 // lowest-index ties: each lane keeps a running maximum over its tokens (read
-// four at a time from LDS), one 64-bit key (value, ~index) per lane is reduced
-// across the wavefront with DPP moves, and the W wavefronts' winners meet in
-// one LDS exchange.  The winner's next state rides along with its key.  No
+// four at a time from LDS), the lanes' (value, index) pairs are reduced
+// across the wavefront with DPP moves (the largest value, then the smallest
+// index holding it), and the W wavefronts' winners meet as 64-bit keys
+// (value, ~index) in one LDS exchange.  The winner's next state rides along with its key.  No
 // MFMA: one fma and one compare per token.
 //
 // The decode kernel keeps each utterance's state and previous label in
@@ -183,7 +184,7 @@ __device__ __forceinline__ int group_argmax(float bx, int bi, int payload, float
                                             Exchange *xc, int &xi, int wave, int lane) {
     static_assert(W == 1 || W == 2 || W == 4, "the exchange area holds at most four wavefronts");
     const unsigned long long mine = argmax_key(bx, bi);
-    unsigned long long k = wave_max_u64(mine);
+    unsigned long long k = wave_argmax_key(bx, bi);
     // the lane whose key won hands over its payload (the lowest such lane: keys are unique but for kNone)
     const unsigned long long won = __builtin_amdgcn_read_exec() & __ballot(mine == k);
     const int src = won ? int(__builtin_ctzll(won)) : 0;
@@ -315,6 +316,8 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     const float *src = asr + b * ld;
     copy_stripes_dword<W>(src, arow, V, wave, lane);
     const float rowV = MODE == kPlain ? 0.0f : src[V];
+    // the previous label is loaded with the state, not after the state's check
+    const int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
     int s = __builtin_amdgcn_readfirstlane(states[b]);
     if (s < 0 || s >= t.num_states) {
         if (wave == 0 && lane == 0) {
@@ -324,7 +327,6 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
     int xi = 0;
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
@@ -522,7 +524,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
                 for (int q = 3; q >= 0; --q)
                     if (n[q] >= 0) lo = v0 + q;
             }
-            w = argmax_index(wave_max_u64(argmax_key(-__builtin_inff(), lo)));
+            w = int(~wave_max_u32(~(unsigned)lo));
         }
         if (lane == ((w & (kStripe - 1)) >> 2)) {   // the lane that owns token w
             otok[j] = w;
@@ -610,7 +612,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
 #pragma unroll
                 for (int j = 3; j >= 0; --j)
                     if (n[c][j] >= 0) lo = c * kStripe + 4 * lane + j;
-            w = argmax_index(wave_max_u64(argmax_key(-__builtin_inff(), lo)));
+            w = int(~wave_max_u32(~(unsigned)lo));
         }
         const int wc = w >> 8, wj = w & 3;   // uniform: the winner's stripe and slot
         if (lane == ((w & (kStripe - 1)) >> 2)) {   // the lane that owns token w

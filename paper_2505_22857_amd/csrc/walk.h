@@ -272,52 +272,60 @@ __device__ __forceinline__ void slot_value(const ChainHead &h, float x, int n, f
     }
 }
 
-// One step of the wave maximum: each lane takes the larger of its key and the
-// key DPP control CTRL moves into it (lanes with no source, or outside
-// ROW_MASK, see 0, which never wins since keys are unsigned).
+// One step of the wave maximum: each lane takes the larger of its value and
+// the value DPP control CTRL moves into it (lanes with no source, or outside
+// ROW_MASK, see 0, which never wins since the values are unsigned).
 template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ unsigned long long max_step(unsigned long long k) {
-    const int lo = int(unsigned(k & 0xffffffffu));
-    const int hi = int(unsigned(k >> 32));
-    const unsigned olo = unsigned(__builtin_amdgcn_update_dpp(0, lo, CTRL, ROW_MASK, 0xf, true));
-    const unsigned ohi = unsigned(__builtin_amdgcn_update_dpp(0, hi, CTRL, ROW_MASK, 0xf, true));
-    const unsigned long long o = (static_cast<unsigned long long>(ohi) << 32) | olo;
+__device__ __forceinline__ unsigned max_step(unsigned k) {
+    const unsigned o = unsigned(__builtin_amdgcn_update_dpp(0, int(k), CTRL, ROW_MASK, 0xf, true));
     return o > k ? o : k;
 }
 
-// Wave-wide maximum of a 64-bit key, uniform in every lane.  An inclusive scan
-// within each row of 16 lanes (row_shr 1, 2, 4, 8), then row 15 broadcast into
-// rows 1 and 3 and row 31 into rows 2 and 3, leaves the maximum in lane 63.
-__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long k) {
+// Wave-wide maximum of an unsigned value, uniform in every lane.  An inclusive
+// scan within each row of 16 lanes (row_shr 1, 2, 4, 8), then row 15
+// broadcast into rows 1 and 3 and row 31 into rows 2 and 3, leaves the
+// maximum in lane 63.
+__device__ __forceinline__ unsigned wave_max_u32(unsigned k) {
     k = max_step<0x111, 0xf>(k);
     k = max_step<0x112, 0xf>(k);
     k = max_step<0x114, 0xf>(k);
     k = max_step<0x118, 0xf>(k);
     k = max_step<0x142, 0xa>(k);
     k = max_step<0x143, 0xc>(k);
-    const unsigned lo = unsigned(__builtin_amdgcn_readlane(int(unsigned(k & 0xffffffffu)), kWave - 1));
-    const unsigned hi = unsigned(__builtin_amdgcn_readlane(int(unsigned(k >> 32)), kWave - 1));
-    return (static_cast<unsigned long long>(hi) << 32) | lo;
+    return unsigned(__builtin_amdgcn_readlane(int(k), kWave - 1));
 }
 
-// Argmax key: larger value first, then smaller index.  -0 counts as +0 so
+// Order-preserving map of a float to an unsigned value; -0 counts as +0 so
 // that equal values tie exactly as under a '>' comparison.
-__device__ __forceinline__ unsigned long long argmax_key(float x, int idx) {
+__device__ __forceinline__ unsigned value_key(float x) {
     if (x == 0.0f) x = 0.0f;
-    unsigned u = __float_as_uint(x);
-    u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-    return ((unsigned long long)u << 32) | (unsigned)(0xffffffffu - (unsigned)idx);
+    const unsigned u = __float_as_uint(x);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ int argmax_index(unsigned long long key) {
-    return (int)(0xffffffffu - (unsigned)(key & 0xffffffffu));
+// Argmax key: larger value first, then smaller index (value key in the high
+// word, ~index in the low word).
+__device__ __forceinline__ unsigned long long argmax_key(float x, int idx) {
+    return ((unsigned long long)value_key(x) << 32) | (unsigned)(~(unsigned)idx);
 }
+
+__device__ __forceinline__ int argmax_index(unsigned long long key) { return (int)(~(unsigned)(key & 0xffffffffu)); }
 
 // The value an argmax key was made from (-0 comes back as +0).
 __device__ __forceinline__ float key_value(unsigned long long key) {
     unsigned u = unsigned(key >> 32);
     u = (u & 0x80000000u) ? (u & 0x7fffffffu) : ~u;
     return __uint_as_float(u);
+}
+
+// Wave maximum of the lanes' argmax keys (value bx, index bi), uniform: the
+// largest value in one 32-bit pass, then the smallest index among the lanes
+// holding it in a second (a lane not holding it offers 0, below every ~index).
+__device__ __forceinline__ unsigned long long wave_argmax_key(float bx, int bi) {
+    const unsigned vk = value_key(bx);
+    const unsigned m = wave_max_u32(vk);
+    const unsigned ik = wave_max_u32(vk == m ? ~(unsigned)bi : 0u);
+    return ((unsigned long long)m << 32) | ik;
 }
 
 // Per-lane running argmax over indices taken in ascending order: a strictly
@@ -335,7 +343,7 @@ __device__ __forceinline__ void take_max(float f, int v, float &bx, int &bi) {
 // Wave argmax of the lanes' (bx, bi): the lowest index among the largest
 // values, and that value.  kNone when every value was -inf.
 __device__ __forceinline__ int wave_argmax(float bx, int bi, float &best) {
-    const unsigned long long k = wave_max_u64(argmax_key(bx, bi));
+    const unsigned long long k = wave_argmax_key(bx, bi);
     best = key_value(k);
     return argmax_index(k);
 }

@@ -418,13 +418,15 @@ def test_fused_larger_batches(dev, B):
         assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
 
 
-@pytest.mark.parametrize("V,B", [(1000, 2400), (1024, 2400), (1025, 600), (1025, 2000), (2048, 1000), (2048, 1500)])
+@pytest.mark.parametrize("V,B", [(40, 10000), (1000, 2400), (1024, 2400), (1025, 600), (1025, 2000), (2048, 1000),
+                                 (2048, 1500)])
 def test_decode_launch_row_placements(dev, V, B):
     """The whole decode with one wavefront per utterance keeps the ASR rows in
     two LDS buffers while every utterance is resident at once with them (on
-    256 CUs with 160 KiB of LDS each: 2304 utterances at V <= 1024, 1792 at
-    V = 1025, 1024 at V = 2048); beyond that in registers up to V = 1024 (with
-    and without a last register chunk cut short by V), else in one LDS buffer.
+    256 CUs with 160 KiB of LDS each: 9984 utterances at V = 40, 2304 at
+    V = 1000 or 1024, 1792 at V = 1025, 1024 at V = 2048); beyond that in
+    registers up to V = 1024 (with and without a last register chunk cut short
+    by V, or with most chunks past V), else in one LDS buffer.
     The cases cover each placement, and the four fusion modes on the register
     paths."""
     m, lm, o = pair(f"V{V}", lambda: generate_model(V, [V, 20000, 15000], 1.0, seed=V, bos_eos=True))

@@ -545,11 +545,13 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     }
 }
 
-// The same selection for V <= 256 * SPL with each lane's 4 * SPL tokens held in
-// registers (fused value and next state, bit 31 marking a token taken or past
-// V): a round's rescan and marking touch registers only.  Register arrays are
-// indexed with compile-time indices only (unrolled loops with a uniform
-// compare), so they stay in registers.
+// The same selection for V <= 256 * SPL with each lane's 4 * SPL fused values
+// and next states held in registers.  A taken token's value becomes -inf (so
+// the owner's rescan is one compare per token) and its bit is set in the
+// lane's mask (the tokens past V start set); the mask only serves the
+// fallback once every remaining value is -inf.  Register arrays are indexed
+// with compile-time indices only (unrolled loops with a uniform compare), so
+// they stay in registers.
 template <int SPL>
 __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                                int64_t ld, float lambda, int k,
@@ -557,6 +559,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
                                                                int32_t *__restrict__ tokens,
                                                                float *__restrict__ scores,
                                                                int32_t *__restrict__ next) {
+    static_assert(4 * SPL <= 32, "the taken mask holds 32 tokens per lane");
     extern __shared__ float lds[];
     const int lane = threadIdx.x;
     const int64_t b = blockIdx.x;
@@ -581,9 +584,10 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
         return;
     }
     const ChainHead h = walk_into_lds(t, s, ls, ln, lane);   // its final wait covers the ASR row too
-    constexpr int kTaken = int32_t(0x80000000u);
-    float f[SPL][4];
-    int n[SPL][4];
+    // value i = 4 c + j of this lane is token 256 c + 4 lane + j
+    float f[4 * SPL];
+    int n[4 * SPL];
+    unsigned taken = 0;
     float bx = -__builtin_inff();
     int bi = kNone;
 #pragma unroll
@@ -597,46 +601,41 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
             float lm;
             int nx;
             slot_value(h, x[j], m[j], lm, nx);
-            f[c][j] = __builtin_fmaf(lambda, lm, a[j]);
-            n[c][j] = v0 + j < V ? nx : kTaken;   // padding past V counts as taken
-            if (v0 + j < V) take_max(f[c][j], v0 + j, bx, bi);
+            const bool in = v0 + j < V;
+            f[4 * c + j] = in ? __builtin_fmaf(lambda, lm, a[j]) : -__builtin_inff();
+            n[4 * c + j] = nx;
+            if (!in) taken |= 1u << (4 * c + j);
+            take_max(f[4 * c + j], v0 + j, bx, bi);
         }
     }
     for (int r = 0; r < k; ++r) {
         float wv;
         int w = wave_argmax(bx, bi, wv);
         if (w == kNone) {   // everything left is -inf: the lowest index not yet taken
-            int lo = kNone;
-#pragma unroll
-            for (int c = SPL - 1; c >= 0; --c)
-#pragma unroll
-                for (int j = 3; j >= 0; --j)
-                    if (n[c][j] >= 0) lo = c * kStripe + 4 * lane + j;
+            const unsigned left = ~taken & (SPL == 8 ? 0xffffffffu : (1u << (4 * SPL)) - 1u);
+            const int i = left ? __builtin_ctz(left) : -1;
+            const int lo = i < 0 ? kNone : (i >> 2) * kStripe + 4 * lane + (i & 3);
             w = int(~wave_max_u32(~(unsigned)lo));
         }
-        const int wc = w >> 8, wj = w & 3;   // uniform: the winner's stripe and slot
+        const int wi = (w >> 8) * 4 + (w & 3);   // uniform: the winner's value index in its owner
         if (lane == ((w & (kStripe - 1)) >> 2)) {   // the lane that owns token w
             float fv = 0.0f;
             int nv = 0;
 #pragma unroll
-            for (int c = 0; c < SPL; ++c)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (c == wc && j == wj) {
-                        fv = f[c][j];
-                        nv = n[c][j];
-                        n[c][j] |= kTaken;
-                    }
+            for (int i = 0; i < 4 * SPL; ++i)
+                if (i == wi) {
+                    fv = f[i];
+                    nv = n[i];
+                    f[i] = -__builtin_inff();
+                }
             otok[r] = w;
             osc[r] = fv;
             onx[r] = nv;
+            taken |= 1u << wi;
             bx = -__builtin_inff();
             bi = kNone;
 #pragma unroll
-            for (int c = 0; c < SPL; ++c)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (n[c][j] >= 0) take_max(f[c][j], c * kStripe + 4 * lane + j, bx, bi);
+            for (int i = 0; i < 4 * SPL; ++i) take_max(f[i], (i >> 2) * kStripe + 4 * lane + (i & 3), bx, bi);
         }
     }
 }

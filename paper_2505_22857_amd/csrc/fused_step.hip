@@ -61,11 +61,11 @@ __device__ __forceinline__ void scan_row(const float *row, int V, int wave, int 
     }
 }
 
-// Per-lane argmax of fmaf(lambda, lm[v], row[v]) over the owned tokens v < V
-// (v != pv in CTC mode), lm[v] from the walked LDS row; same reads as scan_row.
-template <int MODE, int W>
+// Per-lane argmax of fmaf(lambda, lm[v], row[v]) over the owned tokens v < V,
+// lm[v] from the walked LDS row; same reads as scan_row.
+template <int W>
 __device__ __forceinline__ void scan_fused(const ChainHead &h, const float *ls, const int *ln, const float *row,
-                                           float lambda, int pv, int V, int wave, int lane, float &bx, int &bi) {
+                                           float lambda, int V, int wave, int lane, float &bx, int &bi) {
     auto four = [&](int v0, bool tail) {
         const f32x4 x = *reinterpret_cast<const f32x4 *>(ls + v0);
         const i32x4 n = *reinterpret_cast<const i32x4 *>(ln + v0);
@@ -77,7 +77,7 @@ __device__ __forceinline__ void scan_fused(const ChainHead &h, const float *ls, 
             slot_value(h, x[j], n[j], lm, nx);
             const float f = __builtin_fmaf(lambda, lm, a[j]);
             const int v = v0 + j;
-            if ((MODE != kCtc || v != pv) && (!tail || v < V)) take_max(f, v, bx, bi);
+            if (!tail || v < V) take_max(f, v, bx, bi);
         }
     };
     const int full = V & ~(kStripe - 1);
@@ -93,10 +93,9 @@ struct LdsAsr {
     __device__ __forceinline__ void argmax(int V, int wave, int lane, float &bx, int &bi) const {
         scan_row<W>(row, V, wave, lane, bx, bi);
     }
-    template <int MODE>
-    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln, float lambda, int pv,
-                                          int V, int wave, int lane, float &bx, int &bi) const {
-        scan_fused<MODE, W>(h, ls, ln, row, lambda, pv, V, wave, lane, bx, bi);
+    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln, float lambda, int V,
+                                          int wave, int lane, float &bx, int &bi) const {
+        scan_fused<W>(h, ls, ln, row, lambda, V, wave, lane, bx, bi);
     }
 };
 
@@ -142,9 +141,8 @@ struct RegAsr {
             if (FULL || base(i, wave) + kWave <= V || v < V) take_max(a[i], v, bx, bi);
         }
     }
-    template <int MODE>
-    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln, float lambda, int pv,
-                                          int V, int wave, int lane, float &bx, int &bi) const {
+    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln, float lambda, int V,
+                                          int wave, int lane, float &bx, int &bi) const {
 #pragma unroll
         for (int i = 0; i < kN; ++i) {
             const int b0 = base(i, wave);
@@ -154,7 +152,7 @@ struct RegAsr {
             int nx;
             slot_value(h, ls[v], ln[v], lm, nx);
             const float f = __builtin_fmaf(lambda, lm, a[i]);
-            if ((MODE != kCtc || v != pv) && (FULL || b0 + kWave <= V || v < V)) take_max(f, v, bx, bi);
+            if (FULL || b0 + kWave <= V || v < V) take_max(f, v, bx, bi);
         }
     }
 };
@@ -268,9 +266,15 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, flo
         }
     }
     const ChainHead h = walk_record<W>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
+    // CTC: the previous label is no candidate; its slot reads NaN, which no
+    // fused value built from it can pass under a strict '>'
+    if (MODE == kCtc && pv >= 0 && pv < V && owns_token<W>(pv, wave) && lane == 0) {
+        ls[pv] = __builtin_nanf("");
+        ln[pv] = kFinal;
+    }
     float bx = -__builtin_inff(), wv;
     int bi = kNone;
-    asr.template fused<MODE>(h, ls, ln, lambda, pv, V, wave, lane, bx, bi);
+    asr.fused(h, ls, ln, lambda, V, wave, lane, bx, bi);
     // each lane's candidate next state rides along with its key (read from its own stripe)
     int cand = 0;
     if (bi != kNone) {

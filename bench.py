@@ -47,7 +47,7 @@ METRIC = "LM (state,token) scores/s + achieved HBM GB/s for batched advance; fus
 PEAK_HBM_GBPS = 8000.0
 KERNEL_SOURCES = ["paper_2505_22857_amd/csrc/advance.hip", "paper_2505_22857_amd/csrc/walk.h",
                   "paper_2505_22857_amd/csrc/trie.h"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "advance_cfg4_traffic.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "advance_6gram20m_traffic.md")
 
 
 def kernel_source_hash() -> str:
@@ -92,20 +92,20 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="skip the graph of 512-hypothesis calls")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
-              "(the query is replicated per GPU with no exchange, see the design notes)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (a multi-GPU run would "
+              "replicate the trie and split the batch, with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
 
     import torch
 
     import paper_2505_22857_amd as ng
-    from synth import CONFIGS, make_config_model, seed_for, uniform_states
+    from synth import WORKLOADS, make_model, seed_for, uniform_states
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    spec = CONFIGS[4]
+    spec = WORKLOADS["sixgram_20m"]
     t0 = time.time()
-    model = make_config_model(4)
+    model = make_model("sixgram_20m")
     log(f"model generated in {time.time() - t0:.1f}s: counts {model.counts}")
     t0 = time.time()
     lm = ng.NgpuLM.from_model(model)
@@ -116,7 +116,7 @@ def main():
     Bb = spec.batch
     R = args.batches
     B = R * Bb
-    states_np = uniform_states(model, B, seed=seed_for(4) + 1000)
+    states_np = uniform_states(model, B, seed=seed_for("sixgram_20m") + 1000)
     states = torch.from_numpy(states_np).to(dev)
     scores = torch.empty((B, V), dtype=torch.float32, device=dev)
     nxt = torch.empty((B, V), dtype=torch.int32, device=dev)
@@ -228,11 +228,11 @@ def main():
     if args.advance_only:
         return
 
-    # ---- fused greedy CTC step (the config-5 shape), per frame
-    fspec = CONFIGS[5]
+    # ---- fused greedy CTC step (256 utterances x 1000 frames on the 20M 6-gram), per frame
+    fspec = WORKLOADS["ctc_b256_t1000"]
     Bf, T = fspec.batch, args.fused_frames
     g = torch.Generator(device=dev)
-    g.manual_seed(seed_for(5))
+    g.manual_seed(seed_for("ctc_b256_t1000"))
     logits = torch.randn((T, Bf, V + 1), generator=g, device=dev, dtype=torch.float32) * 3.0
     logits[..., V] += fspec.blank_boost
     asr = torch.log_softmax(logits, dim=-1)
@@ -313,7 +313,7 @@ def main():
     # ---- a large batch: 4096 utterances x 200 frames, where the decode is bandwidth-bound
     Bl, Tl = 4096, 200
     gl_ = torch.Generator(device=dev)
-    gl_.manual_seed(seed_for(5) + 20)
+    gl_.manual_seed(seed_for("ctc_b256_t1000") + 20)
     lasr = torch.log_softmax(torch.randn((Bl, Tl, V + 1), generator=gl_, device=dev) * 3.0
                              + torch.nn.functional.one_hot(torch.tensor(V, device=dev), V + 1) * fspec.blank_boost,
                              dim=-1)
@@ -358,9 +358,9 @@ def main():
 
     # ---- beam expansion on the 20M 6-gram: the k best fused tokens of 1024 hypotheses
     Bk = 1024
-    kst = torch.from_numpy(uniform_states(model, Bk, seed=seed_for(5) + 9)).to(dev)
+    kst = torch.from_numpy(uniform_states(model, Bk, seed=seed_for("ctc_b256_t1000") + 9)).to(dev)
     gk = torch.Generator(device=dev)
-    gk.manual_seed(seed_for(5) + 10)
+    gk.manual_seed(seed_for("ctc_b256_t1000") + 10)
     kasr = torch.log_softmax(torch.randn((Bk, V), generator=gk, device=dev) * 3.0, dim=-1)
     topk = {"workload": f"{Bk} hypotheses (256 utterances x beam 4), V={V}, 20M 6-gram, lambda={fspec.lam}"}
     for kk in (4, 32):
@@ -381,15 +381,15 @@ def main():
         f"k=32 {topk['k32_us_per_call']:.1f} us per call")
     del kasr
 
-    # ---- plain fusion on the 200k 4-gram (config 2 shape): B = 32 hypotheses x 200 steps
-    pspec = CONFIGS[2]
-    pmodel = make_config_model(2)
+    # ---- plain fusion on the 200k 4-gram: B = 32 hypotheses x 200 steps
+    pspec = WORKLOADS["fourgram_200k"]
+    pmodel = make_model("fourgram_200k")
     plm = ng.NgpuLM.from_model(pmodel).upload(dev)
     Bp, Tp = pspec.batch, pspec.steps
     gp = torch.Generator(device=dev)
-    gp.manual_seed(seed_for(2))
+    gp.manual_seed(seed_for("fourgram_200k"))
     pasr = torch.log_softmax(torch.randn((Tp, Bp, V), generator=gp, device=dev) * 3.0, dim=-1)
-    pstart = torch.from_numpy(uniform_states(pmodel, Bp, seed=seed_for(2) + 77)).to(dev)
+    pstart = torch.from_numpy(uniform_states(pmodel, Bp, seed=seed_for("fourgram_200k") + 77)).to(dev)
     pst = pstart.clone()
     ptok = torch.empty(Bp, dtype=torch.int32, device=dev)
     for t in range(20):
@@ -433,7 +433,7 @@ def main():
         o.advance(probe, nthreads=cores)
         dt = time.perf_counter() - t0
         n = int(min(1 << 22, max(4096, args.cpu_seconds / max(dt, 1e-6) * len(probe))))
-        sample = uniform_states(model, n, seed=seed_for(4) + 1000)   # starts with the benchmark states
+        sample = uniform_states(model, n, seed=seed_for("sixgram_20m") + 1000)   # starts with the benchmark states
         t0 = time.perf_counter()
         o.advance(sample, nthreads=cores)
         dt = time.perf_counter() - t0
@@ -441,7 +441,7 @@ def main():
                "sample": f"{n} uniform states of the same model (the benchmark draw extended), "
                          f"full {V}-token rows, {dt:.1f}s"}
         log(f"oracle: {cpu['value']:.3g} scores/s on {cores} cores")
-        # the whole config-5 CTC decode (same ASR tensor as the GPU decode above)
+        # the whole 256-utterance CTC decode (same ASR tensor as the GPU decode above)
         from oracle import MODE_CTC
         t0 = time.perf_counter()
         ol, _ = o.decode(asr_host, MODE_CTC, fspec.lam, np.zeros(Bf, np.int32), nthreads=cores)

@@ -12,14 +12,14 @@ the oracle shares arithmetic with it.
 """
 
 from .ngram import NgramModel, generate_model, lookup_ids, state_ids_of
-from .configs import CONFIGS, ConfigSpec, make_config_model, seed_for
+from .configs import WORKLOADS, Workload, make_model, seed_for
 from .workloads import (asr_logprobs, uniform_states, phrase_states,
                         tiny_model, pruned_list)
 from .arpa import write_arpa, write_arpa_list, bpe_like_vocab
 
 __all__ = [
     "NgramModel", "generate_model", "lookup_ids", "state_ids_of",
-    "CONFIGS", "ConfigSpec", "make_config_model", "seed_for",
+    "WORKLOADS", "Workload", "make_model", "seed_for",
     "asr_logprobs", "uniform_states", "phrase_states", "tiny_model",
     "write_arpa", "write_arpa_list", "bpe_like_vocab", "pruned_list",
 ]

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 import paper_2505_22857_amd as ng
-from synth import bpe_like_vocab, generate_model, make_config_model, tiny_model, write_arpa
+from synth import bpe_like_vocab, generate_model, make_model, tiny_model, write_arpa
 
 
 def sorted_list(order, tokens, W, B):
@@ -21,7 +21,7 @@ def sorted_list(order, tokens, W, B):
 
 
 def test_round_trip_plain_model_is_exact():
-    m = make_config_model(1)
+    m = make_model("trigram_v128")
     voc = bpe_like_vocab(m.vocab_size)
     N, o, t, W, B, unk = ng.parse_arpa(write_arpa(m, voc), voc)
     o2, t2, W2, B2 = m.to_list()

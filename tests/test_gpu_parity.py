@@ -17,7 +17,7 @@ torch = pytest.importorskip("torch")
 
 import paper_2505_22857_amd as ng  # noqa: E402
 from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle  # noqa: E402
-from synth import (CONFIGS, asr_logprobs, generate_model, make_config_model, phrase_states,  # noqa: E402
+from synth import (WORKLOADS, asr_logprobs, generate_model, make_model, phrase_states,  # noqa: E402
                    seed_for, tiny_model, uniform_states)
 
 TOL = 1e-5
@@ -49,8 +49,8 @@ def pair(key, make):
     return _PAIRS[key]
 
 
-def cfg_pair(i):
-    return pair(f"cfg{i}", lambda: make_config_model(i))
+def model_pair(key):
+    return pair(key, lambda: make_model(key))
 
 
 def run_advance(lm, states_np, dev):
@@ -81,66 +81,66 @@ def check_advance(name, m, lm, o, states, dev, rows=None):
 
 # ------------------------------------------------------------------ advance
 
-def test_advance_cfg1_every_state(dev):
-    m, lm, o = cfg_pair(1)
-    check_advance("cfg1 all states", m, lm, o, np.arange(m.num_states, dtype=np.int32), dev)
+def test_advance_trigram_every_state(dev):
+    m, lm, o = model_pair("trigram_v128")
+    check_advance("trigram V=128 all states", m, lm, o, np.arange(m.num_states, dtype=np.int32), dev)
 
 
 @pytest.mark.parametrize("B", [1, 33, 32 * 64])
-def test_advance_cfg2(dev, B):
-    m, lm, o = cfg_pair(2)
-    check_advance("cfg2", m, lm, o, uniform_states(m, B, seed=seed_for(2) + B), dev)
+def test_advance_4gram_200k(dev, B):
+    m, lm, o = model_pair("fourgram_200k")
+    check_advance("4-gram 200k", m, lm, o, uniform_states(m, B, seed=seed_for("fourgram_200k") + B), dev)
 
 
-def test_advance_cfg3_deep_phrase_states(dev):
-    m, lm, o = cfg_pair(3)
-    st = phrase_states(m, CONFIGS[3].batch, seed=seed_for(3))
-    check_advance("cfg3 phrase states", m, lm, o, st, dev)
-    check_advance("cfg3 uniform", m, lm, o, uniform_states(m, 1000, seed=seed_for(3) + 1), dev)
+def test_advance_6gram_2m_deep_phrase_states(dev):
+    m, lm, o = model_pair("sixgram_2m_phrases")
+    st = phrase_states(m, WORKLOADS["sixgram_2m_phrases"].batch, seed=seed_for("sixgram_2m_phrases"))
+    check_advance("6-gram 2M phrase states", m, lm, o, st, dev)
+    check_advance("6-gram 2M uniform", m, lm, o, uniform_states(m, 1000, seed=seed_for("sixgram_2m_phrases") + 1), dev)
 
 
-def test_advance_cfg3_rows_normalised(dev):
+def test_advance_6gram_2m_rows_normalised(dev):
     """Every row of 10^5 sampled states sums to one (a property of the generated
     model), on the GPU's scores."""
-    m, lm, o = cfg_pair(3)
-    st = np.concatenate([phrase_states(m, 20000, seed=seed_for(3) + 2),
-                         uniform_states(m, 80000, seed=seed_for(3) + 3)]).astype(np.int32)
-    case(f"advance cfg3 normalisation B={len(st)}")
+    m, lm, o = model_pair("sixgram_2m_phrases")
+    st = np.concatenate([phrase_states(m, 20000, seed=seed_for("sixgram_2m_phrases") + 2),
+                         uniform_states(m, 80000, seed=seed_for("sixgram_2m_phrases") + 3)]).astype(np.int32)
+    case(f"advance 6-gram 2M normalisation B={len(st)}")
     sc, nx = lm.advance(torch.from_numpy(st).to(dev))
     torch.cuda.synchronize()
     assert lm.check_states() == 0
     tot = torch.exp(sc.double()).sum(dim=1)
     err = float((tot - 1).abs().max())
-    print(f"  cfg3 max |sum - 1| over {len(st)} rows: {err:.3g}", flush=True)
+    print(f"  6-gram 2M max |sum - 1| over {len(st)} rows: {err:.3g}", flush=True)
     assert err < 1e-5
     assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
 
 
-def test_advance_cfg4_64_batches_of_512(dev):
+def test_advance_6gram_20m_64_batches_of_512(dev):
     """64 independent 512-hypothesis calls, every row against the oracle."""
-    m, lm, o = cfg_pair(4)
+    m, lm, o = model_pair("sixgram_20m")
     R, Bb = 64, 512
-    states = np.concatenate([uniform_states(m, Bb, seed=seed_for(4) + r) for r in range(R)])
+    states = np.concatenate([uniform_states(m, Bb, seed=seed_for("sixgram_20m") + r) for r in range(R)])
     st = torch.from_numpy(states).to(dev)
     sc = torch.empty((R * Bb, m.vocab_size), dtype=torch.float32, device=dev)
     nx = torch.empty((R * Bb, m.vocab_size), dtype=torch.int32, device=dev)
-    case(f"advance cfg4 {R} calls of B={Bb}")
+    case(f"advance 6-gram 20M {R} calls of B={Bb}")
     for r in range(R):
         sl = slice(r * Bb, (r + 1) * Bb)
         lm.advance(st[sl], sc[sl], nx[sl])
     torch.cuda.synchronize()
     assert lm.check_states() == 0
     o_s32, o_nx, _ = o.advance(states, nthreads=NTHREADS)
-    assert_rows(f"cfg4 {R} x {Bb}", sc.cpu().numpy(), nx.cpu().numpy(), o_s32, o_nx)
+    assert_rows(f"6-gram 20M {R} x {Bb}", sc.cpu().numpy(), nx.cpu().numpy(), o_s32, o_nx)
 
 
-def test_advance_cfg4_bench_launch_sampled(dev):
+def test_advance_6gram_20m_bench_launch_sampled(dev):
     """The benchmark's launch (128 batches of 512 in one call): sampled rows vs the
     oracle, and per-row normalisation (a property of the generated model) on every row."""
-    m, lm, o = cfg_pair(4)
+    m, lm, o = model_pair("sixgram_20m")
     B = 128 * 512
-    states = uniform_states(m, B, seed=seed_for(4) + 1000)
-    case(f"advance cfg4 B={B}")
+    states = uniform_states(m, B, seed=seed_for("sixgram_20m") + 1000)
+    case(f"advance 6-gram 20M B={B}")
     st = torch.from_numpy(states).to(dev)
     sc, nx = lm.advance(st)
     torch.cuda.synchronize()
@@ -149,20 +149,20 @@ def test_advance_cfg4_bench_launch_sampled(dev):
     rows = np.concatenate([rows, [0, B - 1]])
     o_s32, o_nx, _ = o.advance(states[rows], nthreads=NTHREADS)
     rt = torch.from_numpy(rows).to(dev)
-    assert_rows("cfg4 B=65536 sampled", sc[rt].cpu().numpy(), nx[rt].cpu().numpy(), o_s32, o_nx)
+    assert_rows("6-gram 20M B=65536 sampled", sc[rt].cpu().numpy(), nx[rt].cpu().numpy(), o_s32, o_nx)
     tot = torch.exp(sc.double()).sum(dim=1)
     assert float((tot - 1).abs().max()) < 1e-5
     assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
 
 
-@pytest.mark.parametrize("which", ["cfg2", "V1025", "N10"])
+@pytest.mark.parametrize("which", ["4gram_200k", "V1025", "N10"])
 def test_advance_grouped_mapping_with_bad_states(dev, which):
     """Batches of 32768 and more take the XCD-grouped mapping: every row, including
     rows of out-of-range states (written by exactly one owner), vs the oracle.
     N10: a 10-gram, whose order-9 states have chain records longer than the
     scan preloads."""
-    if which == "cfg2":
-        m, lm, o = cfg_pair(2)
+    if which == "4gram_200k":
+        m, lm, o = model_pair("fourgram_200k")
         B = 40000
     elif which == "V1025":
         m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
@@ -228,7 +228,7 @@ def test_repaired_pruned_model(dev):
     decode launch against the oracle on the oracle's own repair of the list."""
     from oracle import repair_list
     from synth import pruned_list
-    m0 = make_config_model(2)
+    m0 = make_model("fourgram_200k")
     o, t, W, B = pruned_list(m0, 0.2, seed=11)
     V, N = m0.vocab_size, m0.max_order
     lm = ng.NgpuLM(V, N, o, t, W, B, m0.unk_logprob, repair=True).upload(dev)
@@ -236,13 +236,13 @@ def test_repaired_pruned_model(dev):
     orc = Oracle(V, N, *R, m0.unk_logprob)
     assert lm.num_states == orc.num_states
     states = np.concatenate([np.arange(0, lm.num_states, 37), [lm.num_states - 1]]).astype(np.int32)
-    check_advance("repaired pruned cfg2", None, lm, orc, states, dev)
+    check_advance("repaired pruned 4-gram 200k", None, lm, orc, states, dev)
     Bq, T = 48, 40
     starts = np.random.default_rng(13).integers(0, lm.num_states, Bq).astype(np.int32)
     asr = asr_logprobs((Bq, T, V + 1), seed=14, blank_boost=1.0)
     for mode in (MODE_PLAIN, MODE_CTC):
         a = asr if mode == MODE_CTC else np.ascontiguousarray(asr[:, :, :V])
-        case(f"repaired pruned cfg2 decode launch mode={mode}")
+        case(f"repaired pruned 4-gram 200k decode launch mode={mode}")
         gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
         ol, os_ = orc.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
         assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
@@ -256,7 +256,7 @@ def test_advance_unigram_and_unk_models(dev):
 
 
 def test_advance_empty_and_out_of_range(dev):
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     case("advance B=0")
     sc, nx = lm.advance(torch.zeros(0, dtype=torch.int32, device=dev))
     assert sc.shape == (0, m.vocab_size)
@@ -301,49 +301,49 @@ def check_decode(name, lm, o, asr, mode, lam, starts, dev):
     return gl, gs
 
 
-def test_fused_plain_cfg1(dev):
-    m, lm, o = cfg_pair(1)
-    spec = CONFIGS[1]
-    asr = asr_logprobs((spec.batch, spec.steps, m.vocab_size), seed=seed_for(1) + 50)
-    check_decode("plain cfg1", lm, o, asr, MODE_PLAIN, spec.lam, np.zeros(spec.batch, np.int32), dev)
+def test_fused_plain_trigram(dev):
+    m, lm, o = model_pair("trigram_v128")
+    spec = WORKLOADS["trigram_v128"]
+    asr = asr_logprobs((spec.batch, spec.steps, m.vocab_size), seed=seed_for("trigram_v128") + 50)
+    check_decode("plain trigram V=128", lm, o, asr, MODE_PLAIN, spec.lam, np.zeros(spec.batch, np.int32), dev)
 
 
-def test_fused_plain_cfg2_with_advance_every_step(dev):
-    m, lm, o = cfg_pair(2)
-    spec = CONFIGS[2]
-    starts = uniform_states(m, spec.batch, seed=seed_for(2) + 77)
-    asr = asr_logprobs((spec.batch, spec.steps, m.vocab_size), seed=seed_for(2) + 50)
-    gl, gs = check_decode("plain cfg2", lm, o, asr, MODE_PLAIN, spec.lam, starts, dev)
+def test_fused_plain_4gram_200k_with_advance_every_step(dev):
+    m, lm, o = model_pair("fourgram_200k")
+    spec = WORKLOADS["fourgram_200k"]
+    starts = uniform_states(m, spec.batch, seed=seed_for("fourgram_200k") + 77)
+    asr = asr_logprobs((spec.batch, spec.steps, m.vocab_size), seed=seed_for("fourgram_200k") + 50)
+    gl, gs = check_decode("plain 4-gram 200k", lm, o, asr, MODE_PLAIN, spec.lam, starts, dev)
     # the advance query at every step's states
     visited = np.concatenate([starts, gs[:, :-1].reshape(-1)]).astype(np.int32)
-    check_advance("cfg2 states along the decode", m, lm, o, visited, dev)
+    check_advance("4-gram 200k states along the decode", m, lm, o, visited, dev)
 
 
-_CFG5 = {}
+_CTC = {}
 
 
-def cfg5_data():
+def ctc_data():
     """Config 5: the ASR tensor and the oracle's decode of it, computed once."""
-    if not _CFG5:
-        m, lm, o = cfg_pair(4)
-        spec = CONFIGS[5]
+    if not _CTC:
+        m, lm, o = model_pair("sixgram_20m")
+        spec = WORKLOADS["ctc_b256_t1000"]
         V = m.vocab_size
-        asr = asr_logprobs((spec.batch, spec.steps, V + 1), seed=seed_for(5), blank_boost=spec.blank_boost)
-        _CFG5["asr"] = asr
-        _CFG5["oracle"] = o.decode(asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), nthreads=NTHREADS)
-    return _CFG5["asr"], _CFG5["oracle"]
+        asr = asr_logprobs((spec.batch, spec.steps, V + 1), seed=seed_for("ctc_b256_t1000"), blank_boost=spec.blank_boost)
+        _CTC["asr"] = asr
+        _CTC["oracle"] = o.decode(asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), nthreads=NTHREADS)
+    return _CTC["asr"], _CTC["oracle"]
 
 
-def test_fused_ctc_cfg5(dev):
-    m, lm, o = cfg_pair(4)
-    spec = CONFIGS[5]
+def test_fused_ctc_256x1000_per_frame(dev):
+    m, lm, o = model_pair("sixgram_20m")
+    spec = WORKLOADS["ctc_b256_t1000"]
     V = m.vocab_size
-    asr, (ol, os_) = cfg5_data()
-    case(f"fused ctc cfg5 per-frame steps B={spec.batch} T={spec.steps}")
+    asr, (ol, os_) = ctc_data()
+    case(f"fused CTC per-frame steps, 20M 6-gram, B={spec.batch} T={spec.steps}")
     gl, gs = gpu_decode(lm, asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), dev)
     assert lm.check_states() == 0
     assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
-    print(f"  cfg5 per-frame: {gl.size} decisions identical, blank labels {(gl == V).mean():.3f}", flush=True)
+    print(f"  CTC 256x1000 per-frame: {gl.size} decisions identical, blank labels {(gl == V).mean():.3f}", flush=True)
 
 
 # ------------------------------------------------------------------ whole decode in one launch
@@ -364,23 +364,23 @@ def gpu_decode_launch(lm, asr_np, mode, lam, starts, dev, lengths=None, prev0=No
             prev.cpu().numpy() if prev is not None else None)
 
 
-def test_decode_launch_ctc_cfg5(dev):
-    m, lm, o = cfg_pair(4)
-    spec = CONFIGS[5]
-    asr, (ol, os_) = cfg5_data()
-    case(f"decode launch ctc cfg5 B={spec.batch} T={spec.steps}")
+def test_decode_launch_ctc_256x1000(dev):
+    m, lm, o = model_pair("sixgram_20m")
+    spec = WORKLOADS["ctc_b256_t1000"]
+    asr, (ol, os_) = ctc_data()
+    case(f"decode launch CTC, 20M 6-gram, B={spec.batch} T={spec.steps}")
     gl, gs, fin, fprev = gpu_decode_launch(lm, asr, MODE_CTC, spec.lam, np.zeros(spec.batch, np.int32), dev)
     assert lm.check_states() == 0
     bad = np.argwhere(gl != ol)
     assert len(bad) == 0, f"labels differ first at {bad[0]}"
     assert np.array_equal(gs, os_)
     assert np.array_equal(fin, os_[:, -1]) and np.array_equal(fprev, ol[:, -1])
-    print(f"  cfg5 one launch: {gl.size} decisions identical", flush=True)
+    print(f"  CTC 256x1000 one launch: {gl.size} decisions identical", flush=True)
 
 
 @pytest.mark.parametrize("mode", [MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER])
 def test_decode_launch_modes_ragged_lengths(dev, mode):
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B, T = 37, 90
     starts = uniform_states(m, B, seed=31)
@@ -403,7 +403,7 @@ def test_fused_larger_batches(dev, B):
     instead of four; at 5000 utterances (more than the 256 CUs hold at once
     with two V = 1024 ASR rows in LDS each) the whole decode keeps the rows in
     registers."""
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     T = 16
     starts = uniform_states(m, B, seed=B)
@@ -454,7 +454,7 @@ def test_decode_launch_time_major_view(dev, V, B):
     buffers, registers with and without a short last chunk) must read only
     the V (+ 1) classes of its own row."""
     if V == 1024:
-        m, lm, o = cfg_pair(2)
+        m, lm, o = model_pair("fourgram_200k")
     else:
         m, lm, o = pair(f"V{V}", lambda: generate_model(V, [V, 20000, 15000], 1.0, seed=V, bos_eos=True))
     T, pad = 9, 7
@@ -481,7 +481,7 @@ def test_decode_launch_time_major_view(dev, V, B):
 def test_decode_launch_resumes_exactly(dev):
     """Two launches over frames [0, 40) and [40, 90), passing states and labels
     back, equal one decode over all 90 frames."""
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B, T, cut = 24, 90, 40
     starts = uniform_states(m, B, seed=41)
@@ -496,7 +496,7 @@ def test_decode_launch_resumes_exactly(dev):
 
 
 def test_decode_launch_bad_start_state(dev):
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     V = m.vocab_size
     asr = asr_logprobs((3, 7, V), seed=43)
     starts = np.array([2, m.num_states, 5], np.int32)
@@ -509,16 +509,16 @@ def test_decode_launch_bad_start_state(dev):
 
 
 def test_fused_transducer_and_ctc_small(dev):
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     starts = uniform_states(m, 64, seed=5)
     asr = asr_logprobs((64, 40, V + 1), seed=6, blank_boost=3.0)
-    check_decode("transducer cfg2", lm, o, asr, MODE_TRANSDUCER, 0.7, starts, dev)
-    check_decode("ctc cfg2", lm, o, asr, MODE_CTC, 0.7, starts, dev)
+    check_decode("transducer 4-gram 200k", lm, o, asr, MODE_TRANSDUCER, 0.7, starts, dev)
+    check_decode("ctc 4-gram 200k", lm, o, asr, MODE_CTC, 0.7, starts, dev)
 
 
 def test_fused_ties_lambda_zero_and_all_blank(dev):
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     V = m.vocab_size
     B = 65
     starts = uniform_states(m, B, seed=8)
@@ -560,7 +560,7 @@ def _edge_frames(V, B):
 
 @pytest.mark.parametrize("mode", [MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER])
 def test_fused_minus_inf_and_lane_ties(dev, mode):
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B = 40
     asr = _edge_frames(V, B)
@@ -623,7 +623,7 @@ def test_max_vocabulary(dev):
 
 def test_fused_strided_asr_rows(dev):
     """asr rows with a leading dimension larger than V + 1."""
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     V = m.vocab_size
     base = asr_logprobs((16, V + 1), seed=10, blank_boost=1.0)
     padded = np.full((16, V + 40), 7.0, np.float32)   # padding must never be read
@@ -643,14 +643,14 @@ def test_fused_strided_asr_rows(dev):
 
 
 @pytest.mark.parametrize("k", [1, 5, 32])
-def test_fused_topk_cfg2(dev, k):
-    m, lm, o = cfg_pair(2)
+def test_fused_topk_4gram_200k(dev, k):
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B = 50
     states = uniform_states(m, B, seed=51 + k)
     asr = asr_logprobs((B, V), seed=52 + k)
     asr[:3] = -7.0                            # full ties: lower index first
-    case(f"fused top-k cfg2 B={B} k={k}")
+    case(f"fused top-k 4-gram 200k B={B} k={k}")
     tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), 0.6, k, torch.from_numpy(states).to(dev))
     torch.cuda.synchronize()
     assert lm.check_states() == 0
@@ -662,7 +662,7 @@ def test_fused_topk_cfg2(dev, k):
 
 @pytest.mark.parametrize("lam", [0.0, 0.6])
 def test_fused_topk_minus_inf_and_ties(dev, lam):
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B, k = 8, 12
     states = uniform_states(m, B, seed=61)
@@ -767,7 +767,7 @@ def test_aed_greedy_step_and_decode(dev):
 
 
 def test_aed_mode_needs_final_weights(dev):
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     asr = torch.zeros((2, m.vocab_size + 1), device=dev)
     st = torch.zeros(2, dtype=torch.int32, device=dev)
     with pytest.raises(ng.NgpuError):
@@ -780,7 +780,7 @@ def test_graph_capture_replays_match_eager(dev):
     """The per-frame steps and an advance captured in one HIP graph (the paper
     runs its decoding steps in CUDA graphs) give the eager results on every
     replay, with eager work in between."""
-    m, lm, o = cfg_pair(2)
+    m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B, T = 32, 12
     asr_np = asr_logprobs((T, B, V + 1), seed=91, blank_boost=2.0)
@@ -852,7 +852,7 @@ def test_graph_capture_replays_match_eager(dev):
 
 def test_fused_zero_sizes(dev):
     """B = 0 (and T = 0 for the decode) launch nothing and change nothing."""
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     V = m.vocab_size
     case("fused entry points with B = 0 / T = 0")
     empty_asr = torch.empty((0, V + 1), device=dev)
@@ -873,7 +873,7 @@ def test_batches_beyond_the_dispatch_limit_are_rejected(dev):
     """B above NGPU_LM_MAX_BATCH (2^26 - 256) is an error for every batched call,
     before any pointer is read."""
     import ctypes
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     big = (1 << 26) - 255
     buf = torch.zeros(1024, dtype=torch.int32, device=dev)
     p = ctypes.c_void_p(buf.data_ptr())
@@ -890,7 +890,7 @@ def test_batches_beyond_the_dispatch_limit_are_rejected(dev):
 def test_binding_rejects_short_asr_rows(dev):
     """The binding checks the class width the C-ABI cannot see: V classes, plus
     blank (or <eos>) outside plain fusion."""
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     V = m.vocab_size
     st = torch.zeros(4, dtype=torch.int32, device=dev)
     prev = torch.full((4,), V, dtype=torch.int32, device=dev)
@@ -911,7 +911,7 @@ def test_binding_rejects_short_asr_rows(dev):
 
 
 def test_fused_out_of_range_state(dev):
-    m, lm, o = cfg_pair(1)
+    m, lm, o = model_pair("trigram_v128")
     V = m.vocab_size
     case("fused with an out-of-range state")
     st = torch.tensor([3, m.num_states + 5, 0], dtype=torch.int32, device=dev)

@@ -15,7 +15,7 @@ import pytest
 
 import paper_2505_22857_amd as ng
 from oracle import Oracle
-from synth import generate_model, make_config_model, tiny_model, uniform_states
+from synth import generate_model, make_model, tiny_model, uniform_states
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "ngpu_lm.h")
@@ -93,12 +93,12 @@ def walk_image(im, s):
     return sc, nxt
 
 
-@pytest.mark.parametrize("which", ["cfg1", "cfg2", "tiny-unk", "n1", "n2", "n10"])
+@pytest.mark.parametrize("which", ["trigram_v128", "fourgram_200k", "tiny-unk", "n1", "n2", "n10"])
 def test_image_walk_matches_oracle(which):
-    if which == "cfg1":
-        m, states = make_config_model(1), None
-    elif which == "cfg2":
-        m = make_config_model(2)
+    if which == "trigram_v128":
+        m, states = make_model("trigram_v128"), None
+    elif which == "fourgram_200k":
+        m = make_model("fourgram_200k")
         states = uniform_states(m, 300, seed=2)
     elif which == "tiny-unk":
         m, states = tiny_model(9, 3, seed=21, n_unigrams=6), None
@@ -170,8 +170,8 @@ def test_bos_eos_build_errors():
 
 
 def test_numbering_matches_oracle_on_shuffled_lists():
-    for idx in (1, 2):
-        m = make_config_model(idx)
+    for idx, key in ((1, "trigram_v128"), (2, "fourgram_200k")):
+        m = make_model(key)
         lm = ng.NgpuLM.from_model(m, shuffle_seed=idx)
         o = Oracle.from_model(m, shuffle_seed=idx + 10)
         S = lm.num_states
@@ -181,7 +181,7 @@ def test_numbering_matches_oracle_on_shuffled_lists():
 
 
 def test_chain_records_and_sparse_rows():
-    m = make_config_model(2)
+    m = make_model("fourgram_200k")
     lm = ng.NgpuLM.from_model(m)
     o = Oracle.from_model(m)
     im = parse_image(lm.host_image())
@@ -256,7 +256,7 @@ def test_build_error_codes():
 
 
 def test_queries_before_upload_fail_cleanly():
-    m = make_config_model(1)
+    m = make_model("trigram_v128")
     lm = ng.NgpuLM.from_model(m)
     lib = ng.load_library()
     assert lib.ngpu_lm_advance(lm._h, None, 4, None, None, None) == -8
@@ -267,7 +267,7 @@ def test_queries_before_upload_fail_cleanly():
 
 
 def test_query_bytes():
-    m = make_config_model(2)
+    m = make_model("fourgram_200k")
     lm = ng.NgpuLM.from_model(m)
     V = m.vocab_size
     hbm, tot = lm.query_bytes(np.zeros(3, np.int32))

@@ -19,7 +19,7 @@ import pytest
 import oracle
 import paper_2505_22857_amd as ng
 from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, Oracle
-from synth import (asr_logprobs, bpe_like_vocab, generate_model, make_config_model, pruned_list, tiny_model,
+from synth import (asr_logprobs, bpe_like_vocab, generate_model, make_model, pruned_list, tiny_model,
                    write_arpa)
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -73,7 +73,7 @@ def _run(cmd):
 
 def _models():
     return {
-        "config1": make_config_model(1),
+        "config1": make_model("trigram_v128"),
         "unk": tiny_model(9, 3, seed=21, n_unigrams=6),
         "bos_eos": generate_model(40, [40, 300, 500, 300], 1.0, seed=5, bos_eos=True),
         "unigram": generate_model(17, [17], 1.0, seed=6),

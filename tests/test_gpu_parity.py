@@ -498,6 +498,8 @@ def test_decode_launch_lambda_signs(dev, B):
             bad = np.argwhere(gl != ol)
             assert len(bad) == 0, f"labels differ first at {bad[0]}"
             assert np.array_equal(gs, os_)
+            if B < 512:   # the per-frame step kernel too
+                check_decode(f"lambda={lam} mode={mode}", lm, o, a, mode, lam, starts, dev)
 
 
 def test_decode_launch_resumes_exactly(dev):

@@ -86,7 +86,7 @@ def test_advance_trigram_every_state(dev):
     check_advance("trigram V=128 all states", m, lm, o, np.arange(m.num_states, dtype=np.int32), dev)
 
 
-@pytest.mark.parametrize("B", [1, 33, 32 * 64])
+@pytest.mark.parametrize("B", [1, 33, 1024, 1025, 32 * 64])
 def test_advance_4gram_200k(dev, B):
     m, lm, o = model_pair("fourgram_200k")
     check_advance("4-gram 200k", m, lm, o, uniform_states(m, B, seed=seed_for("fourgram_200k") + B), dev)
@@ -195,6 +195,28 @@ def test_advance_odd_shapes(dev, V, N):
     if len(st) > 3000:
         st = uniform_states(m, 3001, seed=1)
     check_advance(f"V={V} N={N}", m, lm, o, st, dev)
+
+
+@pytest.mark.parametrize("V,N", [(5, 3), (300, 3), (700, 3), (1025, 4), (4096, 3), (16, 10)])
+def test_advance_small_batches_every_stripe_count(dev, V, N):
+    """Batches of up to 1024 hypotheses run with one wavefront per 256-token
+    stripe, at most four: V = 5 and 16 one stripe, 300 two, 700 three stripes
+    on two wavefronts, 1025 (no 16-byte stores) and 4096 four.  Out-of-range
+    states among them give rows of NaN / -1 and are counted."""
+    if N == 10:
+        counts = [V, 120, 200, 200, 180, 160, 140, 120, 100, 80]
+    else:
+        counts = [V, min(V * V // 2, 6 * V)] + [min(V * V // 2, 6 * V)] * (N - 2)
+    m, lm, o = pair(f"V{V}N{N}", lambda: generate_model(V, counts, 1.0, seed=V + N))
+    st = uniform_states(m, 700, seed=V + 2)
+    st[[3, 400]] = [-1, m.num_states]
+    case(f"advance small batch V={V} N={N} B={len(st)} with 2 bad states")
+    sc, nx = run_advance(lm, st, dev)
+    assert lm.check_states() == 2
+    assert np.isnan(sc[[3, 400]]).all() and (nx[[3, 400]] == -1).all()
+    good = np.setdiff1d(np.arange(len(st)), [3, 400])
+    o_s32, o_nx, _ = o.advance(st[good], nthreads=NTHREADS)
+    assert_rows(f"V={V} N={N} small batch", sc[good], nx[good], o_s32, o_nx)
 
 
 def ten_gram_pair():

@@ -14,7 +14,9 @@
 // in its group; the eight workgroups of a chunk together cover every
 // hypothesis exactly once.  Each XCD's L2 then holds an eighth of the dense
 // rows instead of all of them.  G = 1 is the plain one-hypothesis-per-wave
-// mapping.  No MFMA: the work is gathers, scatters and one fp32 add per token.
+// mapping.  Small batches (latency-bound) give each hypothesis one wavefront
+// per 256-token stripe instead (advance_striped_kernel).  No MFMA: the work is
+// gathers, scatters and one fp32 add per token.
 #include <hip/hip_runtime.h>
 
 #include <cmath>

@@ -896,6 +896,54 @@ def test_graph_capture_replays_match_eager(dev):
     assert np.array_equal(ref[8].cpu().numpy(), ot) and np.array_equal(ref[10].cpu().numpy(), onx)
 
 
+def test_concurrent_streams_match_sequential(dev):
+    """Queries on one uploaded model from four streams at once (advance, a
+    whole decode, per-frame steps and top-k, each on its own buffers) give
+    what they give one after another: the library keeps no per-call state
+    besides the status count."""
+    m, lm, o = model_pair("fourgram_200k")
+    V = m.vocab_size
+    B, T = 96, 20
+    st_adv = torch.from_numpy(uniform_states(m, 700, seed=61)).to(dev)
+    starts = uniform_states(m, B, seed=62)
+    asr = torch.from_numpy(asr_logprobs((B, T, V + 1), seed=63, blank_boost=1.0)).to(dev)
+    rows = [asr[:, t, :].contiguous() for t in range(T)]
+
+    def run(streams):
+        out = {}
+        with torch.cuda.stream(streams[0]):
+            out["adv"] = lm.advance(st_adv, stream=streams[0])
+        with torch.cuda.stream(streams[1]):
+            st = torch.from_numpy(starts).to(dev)
+            prev = torch.full((B,), V, dtype=torch.int32, device=dev)
+            out["dec"] = (lm.fused_greedy_decode(asr, 0.5, st, prev, mode=ng.NGPU_FUSION_CTC, stream=streams[1]), st)
+        with torch.cuda.stream(streams[2]):
+            st2 = torch.from_numpy(starts).to(dev)
+            prev2 = torch.full((B,), V, dtype=torch.int32, device=dev)
+            toks = [lm.fused_greedy_step(r, 0.5, st2, prev2, mode=ng.NGPU_FUSION_CTC, stream=streams[2]).clone()
+                    for r in rows]
+            out["step"] = (torch.stack(toks, 1), st2)
+        with torch.cuda.stream(streams[3]):
+            out["topk"] = lm.fused_topk(rows[0][:, :V].contiguous(), 0.5, 8, torch.from_numpy(starts).to(dev),
+                                        stream=streams[3])
+        torch.cuda.synchronize()
+        return out
+
+    case("four streams at once against one stream")
+    main = torch.cuda.current_stream()
+    seq = run([main] * 4)
+    par = run([torch.cuda.Stream() for _ in range(4)])
+    assert lm.check_states() == 0
+    assert torch.equal(seq["adv"][0], par["adv"][0]) and torch.equal(seq["adv"][1], par["adv"][1])
+    assert torch.equal(seq["dec"][0], par["dec"][0]) and torch.equal(seq["dec"][1], par["dec"][1])
+    assert torch.equal(seq["step"][0], par["step"][0]) and torch.equal(seq["step"][1], par["step"][1])
+    assert all(torch.equal(a, b) for a, b in zip(seq["topk"], par["topk"]))
+    # and the decode and the per-frame steps agree with each other and the oracle
+    assert torch.equal(par["dec"][0], par["step"][0])
+    ol, _ = o.decode(asr.cpu().numpy(), MODE_CTC, 0.5, starts, nthreads=NTHREADS)
+    assert np.array_equal(par["dec"][0].cpu().numpy(), ol)
+
+
 def test_fused_zero_sizes(dev):
     """B = 0 (and T = 0 for the decode) launch nothing and change nothing."""
     m, lm, o = model_pair("trigram_v128")

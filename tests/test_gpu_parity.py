@@ -657,6 +657,14 @@ def test_max_vocabulary(dev):
         gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
         ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
         assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
+    # above 512 utterances: one wavefront each, one LDS row buffer (98 KiB of LDS per workgroup)
+    B2, T2 = 600, 6
+    starts2 = uniform_states(m, B2, seed=18)
+    asr2 = asr_logprobs((B2, T2, V + 1), seed=19, blank_boost=1.0)
+    case(f"V=8192 decode launch B={B2}")
+    gl, gs, _, _ = gpu_decode_launch(lm, asr2, MODE_CTC, 0.5, starts2, dev)
+    ol, os_ = o.decode(asr2, MODE_CTC, 0.5, starts2, nthreads=NTHREADS)
+    assert np.array_equal(gl, ol) and np.array_equal(gs, os_)
     case("V=8192 top-k k=20")
     a0 = np.ascontiguousarray(asr[:, 0, :V])
     tok, sc, nx = lm.fused_topk(torch.from_numpy(a0).to(dev), 0.5, 20, torch.from_numpy(starts).to(dev))

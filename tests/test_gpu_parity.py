@@ -421,10 +421,11 @@ def test_decode_launch_modes_ragged_lengths(dev, mode):
 
 @pytest.mark.parametrize("B", [513, 1100, 5000])
 def test_fused_larger_batches(dev, B):
-    """Batches above 512 hypotheses, which run with one wavefront per hypothesis
-    instead of four; at 5000 utterances (more than the 256 CUs hold at once
-    with two V = 1024 ASR rows in LDS each) the whole decode keeps the rows in
-    registers."""
+    """Batches above 512 hypotheses: the whole decode runs with one wavefront
+    per hypothesis instead of four (the per-frame step from 1025 on, so 513
+    covers its four-wavefront path at that size); at 5000 utterances (more
+    than the 256 CUs hold at once with two V = 1024 ASR rows in LDS each) the
+    whole decode keeps the rows in registers."""
     m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     T = 16

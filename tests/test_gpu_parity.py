@@ -345,7 +345,7 @@ _CTC = {}
 
 
 def ctc_data():
-    """Config 5: the ASR tensor and the oracle's decode of it, computed once."""
+    """The 256 x 1000 CTC workload: the ASR tensor and the oracle's decode of it, computed once."""
     if not _CTC:
         m, lm, o = model_pair("sixgram_20m")
         spec = WORKLOADS["ctc_b256_t1000"]

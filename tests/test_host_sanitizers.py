@@ -73,14 +73,14 @@ def _run(cmd):
 
 def _models():
     return {
-        "config1": make_model("trigram_v128"),
+        "trigram_v128": make_model("trigram_v128"),
         "unk": tiny_model(9, 3, seed=21, n_unigrams=6),
         "bos_eos": generate_model(40, [40, 300, 500, 300], 1.0, seed=5, bos_eos=True),
         "unigram": generate_model(17, [17], 1.0, seed=6),
     }
 
 
-@pytest.mark.parametrize("name", ["config1", "unk", "bos_eos", "unigram"])
+@pytest.mark.parametrize("name", ["trigram_v128", "unk", "bos_eos", "unigram"])
 def test_builder_clean_and_identical(drivers, name):
     bd, _, d = drivers
     m = _models()[name]
@@ -182,7 +182,7 @@ def test_arpa_reader_malformed_text(drivers, text):
     assert rc == e.value.code and rc < 0
 
 
-@pytest.mark.parametrize("name", ["config1", "bos_eos"])
+@pytest.mark.parametrize("name", ["trigram_v128", "bos_eos"])
 def test_oracle_clean_and_identical(drivers, name):
     _, od, d = drivers
     m = _models()[name]

@@ -215,7 +215,7 @@ def test_bruteforce_history_recursion_tiny(oracle_lib):
     check_bruteforce_tiny(oracle.LIB_PATH, seeds=range(6))
 
 
-def test_bruteforce_config1_sampled_histories(oracle_lib):
+def test_bruteforce_trigram_v128_sampled_histories(oracle_lib):
     model = make_model("trigram_v128")
     o = Oracle.from_model(model)
     bf = BruteForce.from_model(model)
@@ -236,17 +236,17 @@ def test_bruteforce_config1_sampled_histories(oracle_lib):
         assert abs(s64[st, v] - bf.score(h, v)) < 1e-9
 
 
-def test_normalisation_config1_all_states(oracle_lib):
+def test_normalisation_trigram_v128_all_states(oracle_lib):
     model = make_model("trigram_v128")
     check_normalisation(oracle.LIB_PATH, model, np.arange(model.num_states, dtype=np.int32))
 
 
-def test_normalisation_config2_sampled(oracle_lib):
+def test_normalisation_fourgram_200k_sampled(oracle_lib):
     model = make_model("fourgram_200k")
     check_normalisation(oracle.LIB_PATH, model, uniform_states(model, 3000, seed=9))
 
 
-def test_normalisation_config3_sampled(oracle_lib):
+def test_normalisation_sixgram_2m_sampled(oracle_lib):
     """The 2M 6-gram with context-biasing phrases: deep phrase states and uniform ones."""
     model = make_model("sixgram_2m_phrases")
     states = np.concatenate([phrase_states(model, 4000, seed=19), uniform_states(model, 16000, seed=20)])
@@ -316,7 +316,7 @@ def test_full_coverage_context_needs_no_backoff(oracle_lib):
     assert (np.delete(s32b[0], miss) == np.delete(w_full, miss)).all()
 
 
-def test_structural_invariants_config2(oracle_lib):
+def test_structural_invariants_fourgram_200k(oracle_lib):
     model = make_model("fourgram_200k")
     o = Oracle.from_model(model)
     states = uniform_states(model, 200, seed=12)
@@ -377,6 +377,44 @@ def test_ctc_lambda_zero_is_textbook_greedy_ctc(oracle_lib):
         adv = [int(labels[b, t]) for t in range(80)
                if labels[b, t] != V and labels[b, t] != (labels[b, t - 1] if t else V)]
         assert adv == collapse(raw[b])
+
+
+def test_decode_is_causal_resumable_and_the_iterated_step(oracle_lib):
+    """Three invariants of a greedy decode, in every mode: frame t depends on
+    frames <= t only (a ragged length cuts the labels, later frames read -1 and
+    keep the state); two decodes that hand over state and last label equal one
+    decode; and the decode equals the single step iterated frame by frame."""
+    plain = make_model("trigram_v128")
+    marked = generate_model(40, [40, 300, 400], 1.0, seed=12, bos_eos=True)
+    rng = np.random.default_rng(5)
+    for model, mode in ((plain, MODE_PLAIN), (plain, MODE_CTC), (plain, MODE_TRANSDUCER), (marked, MODE_AED)):
+        o = Oracle.from_model(model)
+        V = model.vocab_size
+        B, T, cut = 7, 30, 11
+        C = V if mode == MODE_PLAIN else V + 1
+        asr = asr_logprobs((B, T, C), seed=int(mode) + 20, blank_boost=1.5 if mode != MODE_PLAIN else 0.0)
+        starts = rng.integers(0, o.num_states, B).astype(np.int32)
+        full_l, full_s = o.decode(asr, mode, 0.6, starts)
+        # causal: ragged lengths
+        lengths = np.array([0, 1, 5, T, 17, 29, 3], np.int32)
+        l2, s2 = o.decode(asr, mode, 0.6, starts, lengths=lengths)
+        for b, L in enumerate(lengths):
+            assert np.array_equal(l2[b, :L], full_l[b, :L]) and (l2[b, L:] == -1).all()
+            assert np.array_equal(s2[b, :L], full_s[b, :L])
+            assert (s2[b, L:] == (full_s[b, L - 1] if L else starts[b])).all()
+        # resumable: two decodes handing over (state, last label)
+        a1, b1 = o.decode(np.ascontiguousarray(asr[:, :cut]), mode, 0.6, starts)
+        prev = np.ascontiguousarray(a1[:, -1]) if mode == MODE_CTC else None
+        a2, b2 = o.decode(np.ascontiguousarray(asr[:, cut:]), mode, 0.6, np.ascontiguousarray(b1[:, -1]),
+                          prev=prev)
+        assert np.array_equal(np.concatenate([a1, a2], 1), full_l)
+        assert np.array_equal(np.concatenate([b1, b2], 1), full_s)
+        # the single step iterated
+        st = starts.copy()
+        pv = np.full(B, V, np.int32) if mode == MODE_CTC else None
+        for t in range(T):
+            tok = o.greedy_step(np.ascontiguousarray(asr[:, t]), mode, 0.6, st, pv)
+            assert np.array_equal(tok, full_l[:, t]) and np.array_equal(st, full_s[:, t])
 
 
 def test_transducer_lambda_zero_is_raw_argmax(oracle_lib):

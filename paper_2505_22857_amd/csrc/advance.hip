@@ -194,8 +194,10 @@ static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B,
 }
 
 // Launch shapes, from a sweep on the 20M n-gram workload (V = 1024):
-//  - XCD-grouped mapping from 32768 hypotheses on; below that the grouped
-//    scan costs more latency than the cache locality saves.
+//  - XCD-grouped mapping from 20480 hypotheses on; below that the grouped
+//    scan costs more latency than the cache locality saves (grouped against
+//    plain: 48.3 / 46.9 us at 18000, 49.4 / 52.2 at 20480, 62.4 / 70.1 at
+//    28672, 67.5 / 79.3 at 32767).
 //  - One wavefront per workgroup in the grouped mapping: a wavefront that finds
 //    no hypothesis of its group frees its slot (and LDS) at once instead of
 //    waiting for busier wavefronts of its workgroup.
@@ -205,7 +207,7 @@ static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B,
 //    9.4 us at 128 hypotheses, 9.0 against 9.9 at 512, 9.6 against 10.0 at
 //    1024; 10.7 against 10.5 at 1536 and 12.1 against 11.2 at 2048.
 constexpr int64_t kStripedMaxBatch = 1024;
-constexpr int64_t kGroupedMinBatch = 32768;
+constexpr int64_t kGroupedMinBatch = 20480;
 constexpr int kHpbGrouped = 1;
 constexpr int kHpbPlain = 2;
 

@@ -157,7 +157,7 @@ def test_advance_6gram_20m_bench_launch_sampled(dev):
 
 @pytest.mark.parametrize("which", ["4gram_200k", "V1025", "N10"])
 def test_advance_grouped_mapping_with_bad_states(dev, which):
-    """Batches of 32768 and more take the XCD-grouped mapping: every row, including
+    """Batches of 20480 and more take the XCD-grouped mapping: every row, including
     rows of out-of-range states (written by exactly one owner), vs the oracle.
     N10: a 10-gram, whose order-9 states have chain records longer than the
     scan preloads."""
@@ -166,7 +166,7 @@ def test_advance_grouped_mapping_with_bad_states(dev, which):
         B = 40000
     elif which == "V1025":
         m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
-        B = 33001
+        B = 20481
     else:
         m, lm, o = pair("V16N10", lambda: generate_model(16, [16, 120, 200, 200, 180, 160, 140, 120, 100, 80],
                                                           1.0, seed=26))

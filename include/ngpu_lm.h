@@ -40,6 +40,10 @@ extern "C" {
 
 #define NGPU_LM_MAX_ORDER 10      /* the paper's models go up to order 10 */
 #define NGPU_LM_MAX_VOCAB 8192    /* a V-wide score/state row (8 bytes per token) must fit in 64 KiB of LDS */
+/* Most states a model may have: the kernels keep a state id in 30 bits of a
+ * 32-bit word (the two high bits flag how a row slot was filled).  A larger
+ * model is rejected with NGPU_E_TOO_LARGE. */
+#define NGPU_LM_MAX_STATES ((int64_t)1 << 30)
 /* Most hypotheses (or utterances) per call: the launch grid, 64 work-items per
  * hypothesis, must fit a 32-bit dispatch size.  Larger batches return
  * NGPU_E_INVALID_ARG; split them into several calls. */
@@ -120,7 +124,8 @@ typedef struct {
  * ranges and the backoff weights already summed in Algorithm 1's order) and a
  * dense V-wide row per order-1 context (layout in csrc/trie.h).
  * vocab_size: 1..NGPU_LM_MAX_VOCAB; additionally ceil(log2 V') * N <= 128 with
- * V' = V (V + 2 with NGPU_BUILD_BOS_EOS).
+ * V' = V (V + 2 with NGPU_BUILD_BOS_EOS), and at most NGPU_LM_MAX_STATES
+ * states (NGPU_E_TOO_LARGE otherwise).
  * flags: NGPU_BUILD_BOS_EOS and/or NGPU_BUILD_REPAIR_CLOSURE (else
  * NGPU_E_MISSING_PREFIX / NGPU_E_MISSING_SUFFIX for a list that is not closed).
  * The list is read only during the call.
@@ -181,7 +186,8 @@ enum ngpu_fusion_mode {
 /* One greedy shallow-fusion step (Section 2.3) for B hypotheses.
  * d_asr: [B, asr_ld] fp32 ASR log-probabilities; row b holds classes 0..V-1
  *   (tokens) and, for CTC and transducer modes, class V = blank (AED: <eos>);
- *   asr_ld >= V (PLAIN) or >= V + 1.
+ *   asr_ld >= V (PLAIN) or >= V + 1.  Blank is always the last class, so no
+ *   blank index is passed.
  * lambda: LM weight; the fused score of token v is fmaf(lambda, lm[v], asr[v])
  *   (single rounding), lm[v] being the advance score.
  * PLAIN: label = argmax over v < V of the fused score; state <- next[label].
@@ -246,6 +252,13 @@ int ngpu_lm_fused_greedy_decode(const ngpu_lm *lm, const float *d_asr, int64_t B
  * input states the queries enqueued since the last check met.  Returns
  * NGPU_E_BAD_STATE when the count is non-zero. */
 int ngpu_lm_check_states(const ngpu_lm *lm, void *hip_stream, int64_t *bad_count);
+
+/* The same check without the count: synchronises hip_stream and returns
+ * NGPU_E_BAD_STATE (clearing the count) when queries enqueued since the last
+ * check met out-of-range input states, else NGPU_OK.  Every query kernel
+ * performs the range check itself (one compare per hypothesis), so no build
+ * flag enables it. */
+int ngpu_lm_sync_check(const ngpu_lm *lm, void *hip_stream);
 
 /* Algorithmic memory traffic of ngpu_lm_advance on host-side states h_states[B]:
  *   *hbm_bytes   = 8V (output row) + the state's chain record (16 bytes per

@@ -35,7 +35,7 @@ EXPORTED = [
     "ngpu_lm_build", "ngpu_lm_free", "ngpu_lm_info", "ngpu_lm_state_context", "ngpu_lm_device_bytes",
     "ngpu_lm_upload", "ngpu_lm_advance", "ngpu_lm_fused_greedy_step", "ngpu_lm_fused_greedy_decode",
     "ngpu_lm_fused_topk", "ngpu_lm_start_state", "ngpu_lm_final_weights",
-    "ngpu_lm_check_states",
+    "ngpu_lm_check_states", "ngpu_lm_sync_check",
     "ngpu_lm_query_bytes", "ngpu_lm_host_image", "ngpu_lm_last_error",
     "ngpu_arpa_parse", "ngpu_arpa_list", "ngpu_arpa_free",
 ]
@@ -89,6 +89,7 @@ def load_library(path: str = LIB_PATH):
     lib.ngpu_lm_final_weights.argtypes = [vp, vp, i64, vp, vp]
     lib.ngpu_lm_fused_topk.argtypes = [vp, vp, i64, i64, ctypes.c_float, i32, vp, vp, vp, vp, vp]
     lib.ngpu_lm_check_states.argtypes = [vp, vp, ctypes.POINTER(i64)]
+    lib.ngpu_lm_sync_check.argtypes = [vp, vp]
     lib.ngpu_lm_query_bytes.argtypes = [vp, vp, i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]
     lib.ngpu_lm_host_image.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(ctypes.c_size_t)]
     lib.ngpu_arpa_parse.argtypes = [ctypes.c_char_p, ctypes.c_size_t, vp, i32, ctypes.c_uint32,
@@ -271,6 +272,8 @@ class NgpuLM:
             raise ValueError("states/prev must hold B entries")
         if tokens is None:
             tokens = torch.empty(B, dtype=torch.int32, device=asr.device)
+        if tokens.numel() < B:
+            raise ValueError("tokens must hold at least B entries")
         if asr.dtype is not torch.float32 or not asr.is_cuda:
             raise TypeError("asr must be a float32 device tensor")
         _check(self._lib.ngpu_lm_fused_greedy_step(
@@ -285,6 +288,8 @@ class NgpuLM:
         import torch
         if out is None:
             out = torch.empty(states.numel(), dtype=torch.float32, device=states.device)
+        if out.numel() < states.numel():
+            raise ValueError("out must hold one entry per state")
         _check(self._lib.ngpu_lm_final_weights(self._h, _dptr(states, torch.int32, "states"), states.numel(),
                                                _dptr(out, torch.float32, "out"), _stream_handle(stream)))
         return out
@@ -350,6 +355,10 @@ class NgpuLM:
         if rc not in (0, -12):
             _check(rc)
         return int(n.value)
+
+    def sync_check(self, stream=None) -> None:
+        """Raise NgpuError (BAD_STATE) if queries since the last check met out-of-range states."""
+        _check(self._lib.ngpu_lm_sync_check(self._h, _stream_handle(stream)))
 
     def host_image(self) -> np.ndarray:
         """Copy of the host trie image (uint8), the bytes ``upload`` copies to the device."""

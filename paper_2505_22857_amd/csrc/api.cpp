@@ -299,6 +299,11 @@ int ngpu_lm_check_states(const ngpu_lm *lm, void *hip_stream, int64_t *bad_count
     return ok();
 }
 
+int ngpu_lm_sync_check(const ngpu_lm *lm, void *hip_stream) {
+    int64_t bad = 0;
+    return ngpu_lm_check_states(lm, hip_stream, &bad);
+}
+
 int ngpu_lm_host_image(const ngpu_lm *lm, const void **data, size_t *bytes) {
     if (!lm || !data || !bytes) return fail(NGPU_E_INVALID_ARG, "null argument");
     *data = lm->image.data();

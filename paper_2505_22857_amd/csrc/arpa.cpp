@@ -13,6 +13,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
 #include <string>
 #include <new>
 #include <unordered_map>
@@ -89,8 +90,25 @@ int section_of(const Line &ln) {
 
 extern "C" {
 
+static int arpa_parse(const char *text, size_t len, const char *const *vocab, int32_t V, uint32_t flags,
+                      ngpu_arpa **out);
+
+// Host allocations inside the reader may throw; nothing may cross the C ABI.
 int ngpu_arpa_parse(const char *text, size_t len, const char *const *vocab, int32_t V, uint32_t flags,
                     ngpu_arpa **out) {
+    try {
+        return arpa_parse(text, len, vocab, V, flags, out);
+    } catch (const std::bad_alloc &) {
+        if (out) *out = nullptr;   // arpa_parse frees its partial list as the exception leaves it
+        return ngpu::set_error(NGPU_E_NO_MEMORY, "host allocation failed while reading the ARPA text");
+    } catch (const std::exception &e) {
+        if (out) *out = nullptr;
+        return ngpu::set_error(NGPU_E_NO_MEMORY, std::string("ARPA reader: ") + e.what());
+    }
+}
+
+static int arpa_parse(const char *text, size_t len, const char *const *vocab, int32_t V, uint32_t flags,
+                      ngpu_arpa **out) {
     using ngpu::set_error;
     if (!out) return set_error(NGPU_E_INVALID_ARG, "out is null");
     *out = nullptr;
@@ -111,16 +129,13 @@ int ngpu_arpa_parse(const char *text, size_t len, const char *const *vocab, int3
     id.emplace("<s>", kBos);
     id.emplace("</s>", kEos);
 
-    ngpu_arpa *a = new (std::nothrow) ngpu_arpa();
+    std::unique_ptr<ngpu_arpa> a(new (std::nothrow) ngpu_arpa());   // freed on every early return and throw
     if (!a) return set_error(NGPU_E_NO_MEMORY, "out of host memory");
     const char *cur = text, *end = text + len;
     Line ln;
     std::vector<std::string> f;
     std::vector<int64_t> declared(NGPU_LM_MAX_ORDER + 1, -1);
-    auto fail = [&](int code, const std::string &msg) {
-        delete a;
-        return set_error(code, msg);
-    };
+    auto fail = [&](int code, const std::string &msg) { return set_error(code, msg); };
     // header
     bool in_data = false;
     int section = 0;
@@ -201,7 +216,7 @@ int ngpu_arpa_parse(const char *text, size_t len, const char *const *vocab, int3
                                                 std::to_string(k) + "-grams, the file lists " +
                                                 std::to_string(seen[k]));
     a->count = int64_t(a->order.size());
-    *out = a;
+    *out = a.release();
     return set_error(NGPU_OK, "");
 }
 

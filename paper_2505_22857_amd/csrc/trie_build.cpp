@@ -301,6 +301,11 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
         *err = "too many states or arcs for int32 ids";
         return NGPU_E_TOO_LARGE;
     }
+    if (S > NGPU_LM_MAX_STATES) {
+        *err = std::to_string(S) + " states exceed the " + std::to_string(NGPU_LM_MAX_STATES) +
+               " that 30-bit state ids hold";
+        return NGPU_E_TOO_LARGE;
+    }
 
     // ---- host CSR records over the host arc numbering (orders 2..N at arc_base[k])
     std::vector<StateRec> rec(static_cast<size_t>(S));

@@ -38,6 +38,7 @@ constexpr int kWave = 64;
 constexpr int kArcUnroll = 4;                  // arc stripes of 64 lanes loaded before their LDS writes
 constexpr int32_t kFinal = 0x40000000;         // ln bit: slot written by a sparse level
 constexpr int32_t kStateMask = 0x3fffffff;
+static_assert(int64_t(kStateMask) + 1 == NGPU_LM_MAX_STATES, "state ids fit the bits below the flags");
 
 // Waits until every global -> LDS copy (and every other vector memory access)
 // of this wavefront has completed.  The compiler does not reliably order LDS

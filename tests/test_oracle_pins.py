@@ -11,6 +11,7 @@ mistakes in copies of the oracle and checks that some pin catches each one.
 
 import itertools
 import json
+from fractions import Fraction
 import os
 import shutil
 import subprocess
@@ -504,6 +505,71 @@ def test_bos_eos_bruteforce_histories(oracle_lib):
             assert abs(fin[st] - bf.score(h, eos)) < 1e-5
 
 
+def fmaf32(a, x, y):
+    """fmaf(a, x, y) for fp32 operands, rounded once to the nearest fp32 (ties
+    to even): the exact value as a fraction, then the nearer of the two fp32
+    neighbours around its double rounding."""
+    r = Fraction(float(a)) * Fraction(float(x)) + Fraction(float(y))
+    c = np.float32(float(r))
+    best = None
+    for cand in (np.nextafter(c, np.float32(-np.inf)), c, np.nextafter(c, np.float32(np.inf))):
+        if not np.isfinite(cand):
+            continue
+        d = abs(Fraction(float(cand)) - r)
+        if best is None or d < best[0] or (d == best[0] and (int(cand.view(np.uint32)) & 1) == 0):
+            best = (d, cand)
+    return best[1]
+
+
+def aed_hand_model():
+    """Hand bigram model with sentence markers: tokens a = 0, b = 1, <s> = 2,
+    </s> = 3.  Unigrams a (W -1, B -0.5), b (W -2, B 0), <s> (B -0.25),
+    </s> (W -1.5); bigrams '<s> a' (W -0.5) and 'a </s>' (W -0.75).  Every
+    weight and every sum below is a dyadic fraction, exact in fp32.
+    States: 0 root, 1 'a', 2 'b', 3 '<s>' (the start state).  From state 3:
+    a -> -0.5 (listed, next 1), b -> B(<s>) + W(b) = -2.25 (next 2), final
+    weight B(<s>) + W(</s>) = -1.75.  From state 1: a -> B(a) + W(a) = -1.5
+    (next 1), b -> -2.5 (next 2), final weight -0.75 (listed 'a </s>')."""
+    rows = [((0,), -1.0, -0.5), ((1,), -2.0, 0.0), ((2,), -1.0, -0.25), ((3,), -1.5, 0.0),
+            ((2, 0), -0.5, 0.0), ((0, 3), -0.75, 0.0)]
+    order = np.array([len(r[0]) for r in rows], np.int32)
+    tokens = np.full((len(rows), 2), -1, np.int32)
+    for i, r in enumerate(rows):
+        tokens[i, :len(r[0])] = r[0]
+    W = np.array([r[1] for r in rows], np.float32)
+    B = np.array([r[2] for r in rows], np.float32)
+    return (2, 2, order, tokens, W, B)
+
+
+def check_aed_ties(lib_path):
+    """AED (Section 2.3): <eos> is class V, after every token, so an exact tie
+    between a token and <eos> goes to the token (lowest index); <eos> wins only
+    when strictly larger, and then the state stays."""
+    o = Oracle(*aed_hand_model(), lib_path=lib_path, bos_eos=True)
+    assert o.start_state == 3 and o.state_context(3) == (2,)
+    s32, nx, _ = o.advance(np.array([3, 1], np.int32))
+    assert s32.tolist() == [[-0.5, -2.25], [-1.5, -2.5]] and nx.tolist() == [[1, 2], [1, 2]]
+    assert o.final(np.array([3, 1], np.int32)).tolist() == [-1.75, -0.75]
+    cases = [
+        # (state, lambda, asr [a, b, <eos>], label, state after)
+        (3, 0.0, [-3.0, -1.0, -1.0], 1, 2),      # raw tie b = <eos>: b
+        (3, 0.0, [-1.0, -1.0, -1.0], 0, 1),      # three-way tie: a
+        (3, 0.0, [-3.0, -1.0, -0.5], 2, 3),      # <eos> strictly larger: ends, state kept
+        (3, 0.5, [-5.0, -0.5, -0.75], 1, 2),     # fused: b = -1.125 - 0.5, <eos> = -0.875 - 0.75, tie
+        (3, 0.5, [-5.0, -0.5, -0.5], 2, 3),      # <eos> -1.375 above b -1.625
+        (1, 0.5, [-1.0, -3.0, -1.375], 0, 1),    # a = -0.75 - 1, <eos> = -0.375 - 1.375, tie
+        (1, 0.5, [-1.0, -3.0, -1.25], 2, 1),     # <eos> -1.625 above a -1.75
+    ]
+    for s0, lam, row, lab, s1 in cases:
+        st = np.array([s0], np.int32)
+        tok = o.greedy_step(np.array([row], np.float32), MODE_AED, lam, st)
+        assert (int(tok[0]), int(st[0])) == (lab, s1), (s0, lam, row)
+
+
+def test_aed_hand_ties(oracle_lib):
+    check_aed_ties(oracle.LIB_PATH)
+
+
 def test_aed_mode_rules(oracle_lib):
     """lambda = 0: the raw argmax over V tokens and <eos> (class V); <eos> keeps
     the state; otherwise the state follows the token."""
@@ -526,9 +592,10 @@ def test_aed_mode_rules(oracle_lib):
     tok = o.greedy_step(asr, MODE_AED, 0.8, st)
     s32, _, _ = o.advance(states)
     fin = o.final(states)
+    lam = np.float32(0.8)
     for b in range(60):
-        f = np.append(np.float32(0.8) * s32[b] + asr[b, :V], np.float32(0.8) * fin[b] + asr[b, V])
-        assert tok[b] == int(np.argmax(f)) or abs(f.max() - f[tok[b]]) < 1e-6
+        f = [fmaf32(lam, s32[b, v], asr[b, v]) for v in range(V)] + [fmaf32(lam, fin[b], asr[b, V])]
+        assert tok[b] == int(np.argmax(np.array(f, np.float32)))   # first maximal index
 
 
 def test_repair_of_pruned_lists(oracle_lib):
@@ -569,6 +636,7 @@ MUTANTS = {
     "repeat rescored": ("if (a == V || (mode == MODE_CTC && a == *prev)) {", "if (a == V) {"),
     "last index wins ties": ("if (best < 0 || f > bestval) { best = v; bestval = f; }",
                              "if (best < 0 || f >= bestval) { best = v; bestval = f; }"),
+    "<eos> wins ties": ("if (f > bestval) return V;", "if (f >= bestval) return V;"),
     "repair weighs an added n-gram with itself": ("if (!l->added[r] || l->ord[r] < kmax)", "if (1)"),
     "repair adds no suffixes": ("if (!(special && t[k - 1] == V + 1))\n", "if (0)\n"),
 }
@@ -594,6 +662,7 @@ def test_planted_mistake_is_caught(name, tmp_path):
         lambda: check_ctc_rules(lib),
         lambda: check_generator_ids(lib),
         lambda: check_repair(lib, seeds=(6,)),
+        lambda: check_aed_ties(lib),
     ]
     caught = 0
     for chk in checks:

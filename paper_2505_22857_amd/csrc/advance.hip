@@ -112,7 +112,7 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
 // 256-token stripes c with c mod W = w, copies their dense entries, applies
 // the sparse arcs that fall in them and writes them out, so the wavefronts
 // never wait for each other (no barrier) and each writes a W-th of the row.
-template <int W, bool VEC>
+template <int W, bool VEC, bool SPLIT>
 __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, const int32_t *__restrict__ states,
                                                                      int64_t B, float *__restrict__ scores,
                                                                      int32_t *__restrict__ next) {
@@ -137,7 +137,7 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
     }
     int nlev;
     const int4 rec = fetch_record(t, s, lane, nlev);
-    const ChainHead h = walk_record<W>(t, rec, nlev, ls, ln, lane, wave);
+    const ChainHead h = walk_record<W, false, kArcSlots, SPLIT>(t, rec, nlev, ls, ln, lane, wave);
     for (int c = kStripe * wave; c < V; c += kStripe * W) {
         if (VEC) {
             const int v = c + 4 * lane;
@@ -167,16 +167,26 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
     }
 }
 
+// SPLIT when the wavefronts own one stripe each (V in (256 (W - 1), 256 W]):
+// each then loads only its stripe's part of every level.
 template <int W>
 static hipError_t launch_striped(const DevTrie &t, const int32_t *states, int64_t B, float *scores, int32_t *next,
                                  hipStream_t stream, bool vec) {
     const size_t lds = 2 * size_t(lds_row(t.vocab_size)) * sizeof(float);
-    if (vec)
-        hipLaunchKernelGGL((advance_striped_kernel<W, true>), dim3(unsigned(B)), dim3(W * kWave), lds, stream, t,
-                           states, B, scores, next);
+    const bool split = W > 1 && (t.vocab_size + kStripe - 1) / kStripe == W;
+    const dim3 grid(static_cast<unsigned>(B)), block(W * kWave);
+    if (vec && split)
+        hipLaunchKernelGGL((advance_striped_kernel<W, true, true>), grid, block, lds, stream, t, states, B, scores,
+                           next);
+    else if (vec)
+        hipLaunchKernelGGL((advance_striped_kernel<W, true, false>), grid, block, lds, stream, t, states, B, scores,
+                           next);
+    else if (split)
+        hipLaunchKernelGGL((advance_striped_kernel<W, false, true>), grid, block, lds, stream, t, states, B, scores,
+                           next);
     else
-        hipLaunchKernelGGL((advance_striped_kernel<W, false>), dim3(unsigned(B)), dim3(W * kWave), lds, stream, t,
-                           states, B, scores, next);
+        hipLaunchKernelGGL((advance_striped_kernel<W, false, false>), grid, block, lds, stream, t, states, B, scores,
+                           next);
     return hipGetLastError();
 }
 

@@ -59,9 +59,7 @@ ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     t.chain = base + h.off_chain;
     t.dense_w = reinterpret_cast<const float *>(base + h.off_dense_w);
     t.dense_to = reinterpret_cast<const int32_t *>(base + h.off_dense_to);
-    t.arc_tok = reinterpret_cast<const int32_t *>(base + h.off_arc_tok);
-    t.arc_w = reinterpret_cast<const float *>(base + h.off_arc_w);
-    t.arc_to = reinterpret_cast<const int32_t *>(base + h.off_arc_to);
+    t.arcs = reinterpret_cast<const ngpu::Arc *>(base + h.off_arcs);
     t.final_w = h.has_final ? reinterpret_cast<const float *>(base + h.off_final) : nullptr;
     t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + h.off_status);
     t.num_states = int32_t(lm->S);

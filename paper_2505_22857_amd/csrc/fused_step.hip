@@ -30,10 +30,6 @@ namespace ngpu {
 
 enum { kPlain = 0, kCtc = 1, kTransducer = 2, kAed = 3 };
 
-// Word 3 of a raw (unformatted, unswizzled) buffer resource on gfx9-family
-// chips: 32-bit data format; reads past the resource's byte range return 0.
-constexpr int kBufferConfig = 0x00020000;
-
 // Words of an ASR row buffer in LDS: the V tokens rounded up to whole
 // stripes, so that the 16-byte reads of the scans stay inside it.  (Blank or
 // <eos>, class V, travels in a register.)
@@ -240,7 +236,8 @@ __device__ __forceinline__ int first_token_state(const ChainHead &h, const float
 // previous label (CTC).  after_record runs once the chain record's load is
 // issued.  Returns the label and updates s; all lanes of all W wavefronts
 // return the same values.
-template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook>
+template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook, bool LEVELS = false,
+          bool SPLIT = false>
 __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, float rowV, float lambda, int &s,
                                            int pv, float *ls, int *ln, Exchange *xc, int &xi, int wave, int lane,
                                            const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0,
@@ -265,7 +262,9 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, flo
             return a;
         }
     }
-    const ChainHead h = walk_record<W>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
+    const ChainHead h = LEVELS ? walk_record_levels<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n)
+                               : walk_record<W, false, kArcSlots, SPLIT>(t, rec, nlev, ls, ln, lane, wave, pf_src,
+                                                                         pf_dst, pf_n);
     // CTC: the previous label is no candidate; its slot reads NaN, which no
     // fused value built from it can pass under a strict '>'
     if (MODE == kCtc && pv >= 0 && pv < V && owns_token<W>(pv, wave) && lane == 0) {
@@ -299,7 +298,7 @@ __host__ __device__ inline size_t hyp_lds_bytes(int V, int nrows) {
 }
 
 // One fused step; one hypothesis per workgroup of W wavefronts.
-template <int MODE, int W>
+template <int MODE, int W, bool SPLIT = false>
 __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                                 int64_t ld, float lambda,
                                                                 int32_t *__restrict__ states,
@@ -334,7 +333,8 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     int xi = 0;
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
-    const int label = greedy_step<MODE, W, true>(t, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
+    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, false, SPLIT>(
+        t, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
     if (wave == 0 && lane == 0) {
         tokens[b] = label;
         states[b] = s;
@@ -346,7 +346,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
 // asr[b * stride_b + t * stride_t + class]; one utterance per workgroup of W
 // wavefronts.  NB: ASR row buffers in LDS (1 or 2), or 0 for rows held in
 // registers (V <= kRegTokens; FULL: V = kRegTokens).
-template <int MODE, int W, int NB, bool FULL = false>
+template <int MODE, int W, int NB, bool FULL = false, bool SPLIT = false>
 __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                                   int64_t T, int64_t stride_b, int64_t stride_t,
                                                                   const int32_t *__restrict__ lengths, float lambda,
@@ -416,14 +416,15 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
             RegAsr<W, FULL> nxt_r;
             const float *src = more ? pf : row;
             auto load_next = [&]() { nxt_r.load(src, V, wave, lane); };
-            label = greedy_step<MODE, W, false>(t, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr,
-                                                nullptr, 0, load_next);
+            label = greedy_step<MODE, W, false, RegAsr<W, FULL>, decltype(load_next), true, SPLIT>(
+                t, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr, nullptr, 0, load_next);
             cur_r = nxt_r;
         } else {
             float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
             float *nxt = abuf + (kRowBufs == 2 ? ((f + 1) & 1) * rowp : 0);
-            label = greedy_step<MODE, W, false>(t, LdsAsr<W>{cur}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane,
-                                                kRowBufs == 2 ? pf : nullptr, nxt, V);
+            label = greedy_step<MODE, W, false, LdsAsr<W>, NoHook, true, SPLIT>(
+                t, LdsAsr<W>{cur}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, kRowBufs == 2 ? pf : nullptr, nxt,
+                V);
             // one buffer: every read of this frame's row has completed (its values
             // were consumed by the argmax), so the next row can be copied over it
             if (kRowBufs == 1 && pf) copy_stripes_dword<W>(pf, cur, V, wave, lane);
@@ -704,10 +705,24 @@ inline int waves_per_hyp(int64_t B) { return B <= 512 ? 4 : 1; }
 // at 1024; 11.2 against 10.6 at 2048).
 inline int step_waves_per_hyp(int64_t B) { return B <= 1024 ? 4 : 1; }
 
+// Wavefronts that own one 256-token stripe each load only their stripe's part
+// of every sparse level.
+template <int W>
+inline bool stripe_split(const DevTrie &t) {
+    return W > 1 && (t.vocab_size + kStripe - 1) / kStripe == W;
+}
+
 template <int MODE, int W>
 static hipError_t launch_step_w(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda,
                                 int32_t *states, int32_t *prev, int32_t *tokens, hipStream_t stream) {
-    hipLaunchKernelGGL((fused_step_kernel<MODE, W>), dim3(unsigned(B)), dim3(W * kWave),
+    if constexpr (W > 1) {
+        if (stripe_split<W>(t)) {
+            hipLaunchKernelGGL((fused_step_kernel<MODE, W, true>), dim3(unsigned(B)), dim3(W * kWave),
+                               hyp_lds_bytes(t.vocab_size, 1), stream, t, asr, B, ld, lambda, states, prev, tokens);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((fused_step_kernel<MODE, W, false>), dim3(unsigned(B)), dim3(W * kWave),
                        hyp_lds_bytes(t.vocab_size, 1), stream, t, asr, B, ld, lambda, states, prev, tokens);
     return hipGetLastError();
 }
@@ -735,7 +750,15 @@ template <int MODE, int W, int NB, bool FULL = false>
 static hipError_t launch_decode_w(const DevTrie &t, const float *asr, int64_t B, int64_t T, int64_t sb, int64_t st,
                                   const int32_t *lengths, float lambda, int32_t *states, int32_t *prev,
                                   int32_t *labels, int32_t *label_states, hipStream_t stream) {
-    hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB, FULL>), dim3(unsigned(B)), dim3(W * kWave),
+    if constexpr (W > 1) {
+        if (stripe_split<W>(t)) {
+            hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB, FULL, true>), dim3(unsigned(B)), dim3(W * kWave),
+                               hyp_lds_bytes(t.vocab_size, NB), stream, t, asr, B, T, sb, st, lengths, lambda, states,
+                               prev, labels, label_states);
+            return hipGetLastError();
+        }
+    }
+    hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB, FULL, false>), dim3(unsigned(B)), dim3(W * kWave),
                        hyp_lds_bytes(t.vocab_size, NB), stream, t, asr, B, T, sb, st, lengths, lambda, states, prev,
                        labels, label_states);
     return hipGetLastError();

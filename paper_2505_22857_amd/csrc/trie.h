@@ -7,7 +7,7 @@
 //   chain    per state, its whole backoff chain, grouped by order k and
 //            addressed as chain + off_order[k] + (s - first[k]) * 16 * max(k, 1):
 //              ChainHead {dense_row, acc1, acc0, nlev | group << 16}
-//              ChainLevel[nlev] {arc_begin, arc_end, acc}   (orders k, k-1, ..., 2)
+//              ChainLevel[nlev] {arc_begin, arc_end, acc, splits}   (orders k, k-1, ..., 2)
 //            The accumulators are the fp32 left fold of the backoff weights
 //            from the query state downward (Algorithm 1), computed on the host
 //            in the same order the walk would take, so they are bit-identical
@@ -20,9 +20,10 @@
 //            to one of kGroups groups, balanced by the number of states whose
 //            chain ends in it; a query kernel may serve each group from one XCD
 //            so that the group's rows stay in that XCD's L2.
-//   arc_tok  int32 [A3]  arcs of states of order >= 2 (n-grams of order >= 3),
-//   arc_w    float [A3]  sorted by (from_state, token) (Section 2.2)
-//   arc_to   int32 [A3]
+//   arcs     Arc [A3]    arcs of states of order >= 2 (n-grams of order >= 3),
+//                        sorted by (from_state, token) (Section 2.2); one
+//                        12-byte record {token, weight, next state} per arc,
+//                        so 64 lanes read 64 arcs with one load instruction
 //   final    float [S]   with </s> in the model: each state's end-of-sentence
 //                        weight, folded through its backoff chain at build
 //                        time (Section 2.3, AED)
@@ -37,7 +38,7 @@
 
 namespace ngpu {
 
-constexpr uint32_t kImageMagic = 0x324d4c4e;  // "NLM2"
+constexpr uint32_t kImageMagic = 0x334d4c4e;  // "NLM3"
 constexpr size_t kAlign = 256;
 constexpr int32_t kDenseBackoff = int32_t(0x80000000u);  // flag bit in dense_to
 constexpr int kGroups = 8;                                // dense-row groups (one per XCD)
@@ -49,7 +50,7 @@ struct ImageHeader {
     int32_t dense_rows;
     int64_t num_states;
     int64_t num_arcs;            // sparse arcs in the image (orders >= 3)
-    uint64_t off_status, off_chain, off_dense_w, off_dense_to, off_arc_tok, off_arc_w, off_arc_to;
+    uint64_t off_status, off_chain, off_dense_w, off_dense_to, off_arcs;
     uint64_t total_bytes;
     int32_t first[NGPU_LM_MAX_ORDER + 1];       // first state id of each order; first[N] = S
     uint64_t off_order[NGPU_LM_MAX_ORDER];      // chain offset (from the chain section) per order
@@ -68,9 +69,16 @@ struct ChainLevel {
     int32_t begin;
     int32_t end;
     float acc;
-    int32_t pad;
+    uint32_t splits;   // V <= 1024: arcs with token < 256 | < 512 << 9 | < 768 << 19; else 0
 };
 static_assert(sizeof(ChainHead) == 16 && sizeof(ChainLevel) == 16, "chain records are 16-byte units");
+
+struct Arc {
+    int32_t tok;
+    float w;
+    int32_t to;
+};
+static_assert(sizeof(Arc) == 12, "an arc is three words");
 
 // Host-side CSR record (not in the device image): used for byte accounting.
 struct StateRec {
@@ -85,9 +93,7 @@ struct DevTrie {
     const unsigned char *chain;
     const float *dense_w;
     const int32_t *dense_to;
-    const int32_t *arc_tok;
-    const float *arc_w;
-    const int32_t *arc_to;
+    const Arc *arcs;
     const float *final_w;   // nullptr without </s>
     int32_t *status;
     int32_t num_states;

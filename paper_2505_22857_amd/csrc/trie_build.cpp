@@ -360,12 +360,8 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
     off = align_up(off + size_t(R) * size_t(V) * 4);
     h.off_dense_to = off;
     off = align_up(off + size_t(R) * size_t(V) * 4);
-    h.off_arc_tok = off;
-    off = align_up(off + size_t(A3) * 4);
-    h.off_arc_w = off;
-    off = align_up(off + size_t(A3) * 4);
-    h.off_arc_to = off;
-    off = align_up(off + size_t(A3) * 4);
+    h.off_arcs = off;
+    off = align_up(off + size_t(A3) * sizeof(Arc));
     h.has_final = special ? 1 : 0;
     h.off_final = special ? off : 0;
     if (special) off = align_up(off + size_t(S) * 4);
@@ -384,9 +380,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
     unsigned char *chain = img.data() + h.off_chain;
     float *dense_w = reinterpret_cast<float *>(img.data() + h.off_dense_w);
     int32_t *dense_to = reinterpret_cast<int32_t *>(img.data() + h.off_dense_to);
-    int32_t *arc_tok = reinterpret_cast<int32_t *>(img.data() + h.off_arc_tok);
-    float *arc_w = reinterpret_cast<float *>(img.data() + h.off_arc_w);
-    int32_t *arc_to = reinterpret_cast<int32_t *>(img.data() + h.off_arc_to);
+    Arc *arcs = reinterpret_cast<Arc *>(img.data() + h.off_arcs);
 
     // dense row 0: the empty context (Section 2.2: every token has an arc; missing ones get <unk>)
     for (int32_t v = 0; v < V; ++v) {
@@ -419,9 +413,9 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
         const OrderLevel &L = lv[k];
         for (size_t p = 0; p < L.key.size(); ++p) {
             int64_t a = arc_base[k] - arc3 + int64_t(p);
-            arc_tok[a] = int32_t(uint64_t(L.key[p]) & tmask);
-            arc_w[a] = L.w[p];
-            arc_to[a] = k < N ? int32_t(first[k] + int64_t(p)) : int32_t(first[N - 1] + L.suffix[p]);
+            arcs[a].tok = int32_t(uint64_t(L.key[p]) & tmask);
+            arcs[a].w = L.w[p];
+            arcs[a].to = k < N ? int32_t(first[k] + int64_t(p)) : int32_t(first[N - 1] + L.suffix[p]);
         }
     }
     // dense-row groups: longest-processing-time assignment of rows, weighted by
@@ -452,6 +446,23 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
         }
     }
 
+    // token-stripe splits of each state's arcs (V <= 1024 only): the number of
+    // arcs with token below 256, 512 and 768, packed as 9 + 10 + 10 bits, so
+    // that a query split over the 256-token stripes finds its part of a level
+    // without searching (arcs are sorted by token)
+    std::vector<uint32_t> splits;
+    if (V <= 4 * 256) {
+        splits.assign(size_t(S), 0u);
+        for (int64_t st = first[2 < N ? 2 : N]; N >= 3 && st < S; ++st) {
+            uint32_t c[3] = {0, 0, 0};
+            for (int32_t a = rec[st].begin; a < rec[st].end; ++a) {
+                const int32_t tok = arcs[a - arc3].tok;
+                for (int i = 0; i < 3; ++i) c[i] += tok < 256 * (i + 1) ? 1u : 0u;
+            }
+            splits[size_t(st)] = c[0] | (c[1] << 9) | (c[2] << 19);
+        }
+    }
+
     // chain records: the fp32 fold of backoff weights from the state downward
     {
         ChainHead root{0, 0.0f, 0.0f, row_group[0] << 16};   // the empty context: dense row 0, no sparse level
@@ -468,7 +479,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
                 lev[j].begin = int32_t(rec[s].begin - arc3);
                 lev[j].end = int32_t(rec[s].end - arc3);
                 lev[j].acc = acc;
-                lev[j].pad = 0;
+                lev[j].splits = splits.empty() ? 0u : splits[size_t(s)];
                 acc = acc + rec[s].bw;
                 s = rec[s].bto;
             }

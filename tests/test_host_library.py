@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(lib):
     assert sorted(ng.EXPORTED) == decl
 
 
-HDR_FMT = "<IiiiqqQQQQQQQQ11i4x10QQii"
+HDR_FMT = "<IiiiqqQQQQQQ11i4x10QQii"
 
 
 def parse_image(img):
@@ -48,16 +48,17 @@ def parse_image(img):
     raw = img.tobytes()
     f = struct.unpack_from(HDR_FMT, raw)
     magic, V, N, R, S, A3 = f[:6]
-    o_st, o_ch, o_dw, o_dt, o_tok, o_w, o_to, total = f[6:14]
-    first = list(f[14:25])
-    off_order = list(f[25:35])
-    off_final, start_state, has_final = f[35:38]
-    assert magic == 0x324D4C4E and total == len(img)
+    o_st, o_ch, o_dw, o_dt, o_arc, total = f[6:12]
+    first = list(f[12:23])
+    off_order = list(f[23:33])
+    off_final, start_state, has_final = f[33:36]
+    assert magic == 0x334D4C4E and total == len(img)
+    arcs = np.frombuffer(raw, np.int32, 3 * A3, o_arc).reshape(A3, 3)   # {token, weight bits, next state}
     return dict(V=V, N=N, R=R, S=S, A=A3, first=first, off_order=off_order, raw=raw, o_ch=o_ch,
                 dense_w=np.frombuffer(raw, np.float32, R * V, o_dw).reshape(R, V),
                 dense_to=np.frombuffer(raw, np.int32, R * V, o_dt).reshape(R, V),
-                tok=np.frombuffer(raw, np.int32, A3, o_tok), w=np.frombuffer(raw, np.float32, A3, o_w),
-                to=np.frombuffer(raw, np.int32, A3, o_to), start_state=start_state,
+                tok=arcs[:, 0].copy(), w=arcs[:, 1].copy().view(np.float32), to=arcs[:, 2].copy(),
+                start_state=start_state,
                 final=np.frombuffer(raw, np.float32, S, off_final) if has_final else None)
 
 

@@ -12,9 +12,11 @@ second over the timed steps.  The same run also reports:
   mean kernel duration from HIP events on the launch stream, against 8 TB/s;
   ``traffic`` is the measured HBM bytes per launch from the committed rocprofv3
   counter summary when it was taken on the current kernel source, else null;
-* latency of a single 512-hypothesis call (median of 100);
+* latency of a single 512-hypothesis call (median of 100), with its
+  algorithmic bytes as a fraction of the HBM roofline (roofline_b512_single);
 * the same work as 128 separate 512-hypothesis calls on 8 streams, captured in
-  one HIP graph;
+  one HIP graph, likewise against the roofline (roofline_b512_graph);
+* the transducer mode, one launch per step, at 32 and 256 hypotheses;
 * the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame,
   and the same decode of 1000 frames as one launch;
 * the same decode at B = 4096 utterances x 200 frames, with its algorithmic
@@ -162,6 +164,12 @@ def main():
     torch.cuda.synchronize()
     lat_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in lat]))
     log(f"single B={Bb} call: median {lat_us:.1f} us")
+    # algorithmic bytes of one 512-hypothesis call: the mean over the slices the 100 calls cycle through
+    call_bytes = float(np.mean([lm.query_bytes(states_np[(r % R) * Bb:(r % R + 1) * Bb])[0] for r in range(100)]))
+    single = {"bound": "hbm", "achieved": call_bytes / (lat_us * 1e-6) / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+              "frac": call_bytes / (lat_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, "bytes_per_call": call_bytes,
+              "us_per_call": lat_us,
+              "workload": f"one advance call of B={Bb} uniform states (median of 100, HIP events around the call)"}
 
     # ---- sustained: one launch over all R batches per step
     for _ in range(args.warmup):
@@ -220,8 +228,9 @@ def main():
         assert lm.check_states() == 0
         g_ms = g0.elapsed_time(g1) / reps
         graph = {"workload": f"{R} calls of B={Bb} on 8 streams, one HIP graph replay",
-                 "ms": g_ms, "scores_per_s": B * V / (g_ms * 1e-3),
-                 "algorithmic_gbps": hbm_bytes / (g_ms * 1e-3) / 1e9}
+                 "bound": "hbm", "achieved": hbm_bytes / (g_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                 "frac": hbm_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, "bytes_per_replay": hbm_bytes,
+                 "ms": g_ms, "scores_per_s": B * V / (g_ms * 1e-3)}
         log(f"advance as {R} graph-captured B={Bb} calls on 8 streams: {g_ms:.3f} ms per replay, "
             f"{graph['scores_per_s']:.3g} scores/s")
         del g_adv
@@ -260,6 +269,28 @@ def main():
              "steps_per_s": T / (f_ms * 1e-3), "frames_per_s": Bf * T / (f_ms * 1e-3),
              "us_per_step": f_ms * 1e3 / T}
     log(f"fused CTC: {fused['us_per_step']:.1f} us/step, {fused['frames_per_s']:.3g} frames/s")
+
+    # ---- transducer mode, one launch per step (the LM consulted on non-blank frames), B = 32 and 256
+    transducer = {"workload": f"transducer, 20M 6-gram, {V + 1} classes (log_softmax of N(0,3) logits, blank +"
+                              f"{fspec.blank_boost}), lambda={fspec.lam}, one launch per step, 200 steps"}
+    for Bt in (32, 256):
+        tst = torch.zeros(Bt, dtype=torch.int32, device=dev)
+        ttok = torch.empty((200, Bt), dtype=torch.int32, device=dev)
+        trows = [asr[t, :Bt] for t in range(200)]
+        for t in range(20):
+            lm.fused_greedy_step(trows[t], fspec.lam, tst, mode=ng.NGPU_FUSION_TRANSDUCER, tokens=ttok[t])
+        tst.zero_()
+        torch.cuda.synchronize()
+        f0.record(stream)
+        for t in range(200):
+            lm.fused_greedy_step(trows[t], fspec.lam, tst, mode=ng.NGPU_FUSION_TRANSDUCER, tokens=ttok[t])
+        f1.record(stream)
+        torch.cuda.synchronize()
+        transducer[f"b{Bt}_us_per_step"] = f0.elapsed_time(f1) * 1e3 / 200
+        transducer[f"b{Bt}_lm_share"] = float((ttok != V).float().mean())
+    assert lm.check_states() == 0
+    log(f"fused transducer: {transducer['b32_us_per_step']:.1f} us/step at B=32, "
+        f"{transducer['b256_us_per_step']:.1f} us/step at B=256")
 
     # ---- the same per-frame launches replayed from one HIP graph (decoding steps in a graph)
     if not args.no_graph:
@@ -470,12 +501,14 @@ def main():
                      "total_bytes_per_launch": total_bytes,
                      "total_gbps": total_bytes / (mean_ms * 1e-3) / 1e9},
         "latency_b512_us": lat_us,
+        "roofline_b512_single": single,
+        "roofline_b512_graph": graph,
+        "fused_transducer": transducer,
         "fused": fused,
         "fused_decode": fused_decode,
         "fused_decode_large": fused_large,
         "fused_plain": fused_plain,
         "fused_topk": topk,
-        "advance_graph_b512": graph,
         "cpu_baseline": cpu,
         "cpu_baseline_decode": cpu_decode,
         "kernel_source_sha256": kernel_source_hash(),

@@ -137,7 +137,7 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
     }
     int nlev;
     const int4 rec = fetch_record(t, s, lane, nlev);
-    const ChainHead h = walk_record<W, false, kArcSlots, SPLIT>(t, rec, nlev, ls, ln, lane, wave);
+    const ChainHead h = walk_record<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave);
     for (int c = kStripe * wave; c < V; c += kStripe * W) {
         if (VEC) {
             const int v = c + 4 * lane;

@@ -236,8 +236,7 @@ __device__ __forceinline__ int first_token_state(const ChainHead &h, const float
 // previous label (CTC).  after_record runs once the chain record's load is
 // issued.  Returns the label and updates s; all lanes of all W wavefronts
 // return the same values.
-template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook, bool LEVELS = false,
-          bool SPLIT = false>
+template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook, bool SPLIT = false>
 __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, float rowV, float lambda, int &s,
                                            int pv, float *ls, int *ln, Exchange *xc, int &xi, int wave, int lane,
                                            const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0,
@@ -262,9 +261,7 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, flo
             return a;
         }
     }
-    const ChainHead h = LEVELS ? walk_record_levels<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n)
-                               : walk_record<W, false, kArcSlots, SPLIT>(t, rec, nlev, ls, ln, lane, wave, pf_src,
-                                                                         pf_dst, pf_n);
+    const ChainHead h = walk_record<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
     // CTC: the previous label is no candidate; its slot reads NaN, which no
     // fused value built from it can pass under a strict '>'
     if (MODE == kCtc && pv >= 0 && pv < V && owns_token<W>(pv, wave) && lane == 0) {
@@ -333,7 +330,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     int xi = 0;
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
-    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, false, SPLIT>(
+    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, SPLIT>(
         t, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
     if (wave == 0 && lane == 0) {
         tokens[b] = label;
@@ -416,13 +413,13 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
             RegAsr<W, FULL> nxt_r;
             const float *src = more ? pf : row;
             auto load_next = [&]() { nxt_r.load(src, V, wave, lane); };
-            label = greedy_step<MODE, W, false, RegAsr<W, FULL>, decltype(load_next), true, SPLIT>(
+            label = greedy_step<MODE, W, false, RegAsr<W, FULL>, decltype(load_next), SPLIT>(
                 t, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr, nullptr, 0, load_next);
             cur_r = nxt_r;
         } else {
             float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
             float *nxt = abuf + (kRowBufs == 2 ? ((f + 1) & 1) * rowp : 0);
-            label = greedy_step<MODE, W, false, LdsAsr<W>, NoHook, true, SPLIT>(
+            label = greedy_step<MODE, W, false, LdsAsr<W>, NoHook, SPLIT>(
                 t, LdsAsr<W>{cur}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, kRowBufs == 2 ? pf : nullptr, nxt,
                 V);
             // one buffer: every read of this frame's row has completed (its values

@@ -10,14 +10,17 @@
 //      j the entry of level j - 1.  The record's length follows from s alone
 //      (its order), so nothing waits on the head to fetch the levels.
 //   2. the dense row of the order-1 ancestor (which already folds in the
-//      empty context) is copied global -> LDS by the load unit into the row,
-//      together with the first stripe of sparse arcs (or, when the caller
-//      already knows the dense row from the chain head, before the record
-//      load: walk_into_lds_dense_first).
+//      empty context) is copied global -> LDS by the load unit into the row
+//      (when the caller already knows the dense row from the chain head, before
+//      the record load: walk_into_lds_dense_first).
 //   3. the sparse levels are applied bottom-up (order 2 first, the query
 //      state's order last), each overwriting the slots of its tokens with the
 //      final score and the next state marked kFinal, so the highest order that
-//      holds a token wins, as in Algorithm 1.
+//      holds a token wins, as in Algorithm 1.  Arcs are 12-byte records: up to
+//      four 64-arc stripes of a level are loaded (one load per lane each)
+//      before any of them is written.  When the W wavefronts of a hypothesis
+//      own one 256-token stripe each, every wavefront loads only the arcs of
+//      its stripe, a contiguous part of each level (arcs are sorted by token).
 //   4. the reader turns each slot into (score, next): kFinal slots as they are,
 //      raw dense slots as acc + weight with acc = acc0 where the dense entry is
 //      flagged as backed off to the empty context, else acc1.
@@ -45,6 +48,11 @@ static_assert(int64_t(kStateMask) + 1 == NGPU_LM_MAX_STATES, "state ids fit the 
 // here first; the memory clobber keeps the compiler from moving any memory
 // access across the wait.
 __device__ __forceinline__ void wait_lds_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// vmcnt(0) as an instruction the compiler's wait insertion accounts for
+// (expcnt and lgkmcnt at their maximum: no wait on them); for waits on
+// loads into registers, whose data dependences already order their users.
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 typedef __attribute__((address_space(1))) const void global_cptr;
 typedef __attribute__((address_space(3))) void lds_ptr;
@@ -134,23 +142,6 @@ __device__ __forceinline__ bool owns_token(int tok, int wave) {
     return W == 1 || ((tok >> 8) & (W - 1)) == wave;
 }
 
-// Sparse arcs go in stripes of 64 consecutive arcs of one level, the levels'
-// stripes in walk order (entry nlev, order 2, first; entry 1, the query
-// state, last).  A cursor walks that sequence; the walk loads up to U stripes
-// (one 12-byte load per lane each) before it writes any of them into LDS, so a
-// chain of up to U stripes costs one memory round trip whatever its number of
-// levels.  Each stripe holds one level's arcs, whose tokens are distinct, and
-// stripes are written in walk order, so a token held by several levels ends
-// with the entry of the highest order, as in Algorithm 1.
-constexpr int kArcSlots = 16;   // stripes (of 64 arcs) loaded per round trip by default
-
-struct LevelCursor {
-    int j;       // record entry of the current level (nlev .. 1); 0 once every level is done
-    int a0;      // first arc of the next stripe
-    int end;     // end of the current level's arc range
-    float acc;   // the current level's accumulator
-};
-
 // Arc range of record entry j for wavefront `wave` of W: the whole level, or,
 // when SPLIT (the wavefronts own one 256-token stripe each), the part of it
 // whose tokens fall in the wavefront's stripe, from the level's split counts.
@@ -169,96 +160,9 @@ __device__ __forceinline__ void level_bounds(const int4 &rec, int j, int wave, i
     }
 }
 
-// Moves the cursor past exhausted (or empty) levels; all values uniform.
-template <int W, bool SPLIT>
-__device__ __forceinline__ void cursor_settle(LevelCursor &c, const int4 &rec, int wave) {
-    while (c.j >= 1 && c.a0 >= c.end) {
-        --c.j;
-        if (c.j >= 1) {
-            level_bounds<W, SPLIT>(rec, c.j, wave, c.a0, c.end);
-            c.acc = __int_as_float(__builtin_amdgcn_readlane(rec.z, c.j));
-        }
-    }
-}
-
-template <int W, bool SPLIT>
-__device__ __forceinline__ LevelCursor cursor_start(const int4 &rec, int nlev, int wave) {
-    LevelCursor c{nlev, 0, 0, 0.0f};
-    if (nlev >= 1) {
-        level_bounds<W, SPLIT>(rec, nlev, wave, c.a0, c.end);
-        c.acc = __int_as_float(__builtin_amdgcn_readlane(rec.z, nlev));
-    }
-    cursor_settle<W, SPLIT>(c, rec, wave);
-    return c;
-}
-
 // Word 3 of a raw (unformatted, unswizzled) buffer resource on gfx9-family
 // chips: 32-bit data format; reads past the resource's byte range return 0.
 constexpr int kBufferConfig = 0x00020000;
-
-typedef unsigned u32x3 __attribute__((ext_vector_type(3)));
-
-// One pass over up to U stripes: their layout (uniform values), then one load
-// per stripe through a buffer resource that ends at the stripe's last arc,
-// with no branch around the loads (lanes past the end, and stripes past the
-// chain's last, read zeros), so all U loads are in flight before any wait.  A
-// zero arc is no arc: every arc of order >= 3 leads to a state of order >= 2,
-// never to state 0.
-template <int U>
-struct ArcPass {
-    u32x3 arc[U];
-    float acc[U];
-};
-
-template <int W, bool SPLIT, int U>
-__device__ __forceinline__ void issue_pass(const DevTrie &t, const int4 &rec, LevelCursor &c, int lane, int wave,
-                                           ArcPass<U> &p) {
-    int first[U], count[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        first[u] = 0;
-        count[u] = 0;
-        p.acc[u] = 0.0f;
-        if (c.j >= 1) {
-            first[u] = c.a0;
-            count[u] = c.end - c.a0 < kWave ? c.end - c.a0 : kWave;
-            p.acc[u] = c.acc;
-            c.a0 += kWave;
-            cursor_settle<W, SPLIT>(c, rec, wave);
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<Arc *>(t.arcs + first[u]), short(0), count[u] * int(sizeof(Arc)), kBufferConfig);
-        p.arc[u] = __builtin_amdgcn_raw_buffer_load_b96(r, lane * int(sizeof(Arc)), 0, 0);
-    }
-}
-
-// The pass's arcs into LDS, the tokens owned by wavefront `wave` of W.
-template <int W, int U>
-__device__ __forceinline__ void write_pass(const ArcPass<U> &p, float *ls, int *ln, int wave) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const int tok = int(p.arc[u].x), to = int(p.arc[u].z);
-        if (to != 0 && owns_token<W>(tok, wave)) {
-            ls[tok] = p.acc[u] + __uint_as_float(p.arc[u].y);
-            ln[tok] = to | kFinal;
-        }
-    }
-}
-
-// Stripes of the record's sparse levels that wavefront `wave` loads (uniform).
-template <int W, bool SPLIT>
-__device__ __forceinline__ int chain_stripes(const int4 &rec, int nlev, int wave) {
-    int q = 0;
-    for (int j = 1; j <= nlev; ++j) {
-        int a0, end;
-        level_bounds<W, SPLIT>(rec, j, wave, a0, end);
-        q += (end - a0 + kWave - 1) / kWave;
-    }
-    return q;
-}
 
 // Issues the load of state s's chain record (s uniform and valid); nlev is its
 // number of levels.  The record is consumed by walk_record().
@@ -303,40 +207,19 @@ __device__ __forceinline__ void dense_stripes_to_lds(const DevTrie &t, int row, 
     }
 }
 
-// First pass of the walk: the arc loads of up to U stripes, then the global ->
-// LDS copies (dense row unless DENSE_ISSUED, and the prefetch), then one wait
-// for all of them, then the arcs' LDS writes.  The copies go last because the
-// compiler waits for every load in flight before it reuses a copy's address
-// registers, and the arc writes must land on top of the copied dense row.
-template <int W, bool SPLIT, int U, bool DENSE_ISSUED>
-__device__ __forceinline__ void walk_first_pass(const DevTrie &t, const int4 &rec, LevelCursor &c, int dense_row,
-                                                float *ls, int *ln, int lane, int wave, const float *pf_src,
-                                                float *pf_dst, int pf_n) {
-    ArcPass<U> p;
-    issue_pass<W, SPLIT, U>(t, rec, c, lane, wave, p);
-    if (!DENSE_ISSUED) dense_stripes_to_lds<W>(t, dense_row, ls, ln, wave, lane);
-    if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
-    wait_lds_copies();
-    write_pass<W, U>(p, ls, ln, wave);
-}
-
 // The walk of a fetched record into (ls, ln), the stripes of wavefront `wave`
-// of W.  When pf_src is given, pf_n words from it are also copied into pf_dst
-// (the owned stripes) once the record is in (a prefetch that rides along with
-// the dense row and the arcs).  DENSE_ISSUED: the caller already issued the
-// copy of the dense row.  A chain of up to UMAX stripes costs one memory round
-// trip whatever its number of levels; the first pass takes as few stripe
-// slots as the chain needs (2, 4, 8 or UMAX), since every slot issues a load.
-// The walk of a fetched record into (ls, ln), level by level in walk order,
-// up to four stripes of a level per memory round trip.  Its code is a fraction
-// of walk_record's, which is what a loop that walks once per frame wants.
-template <int W = 1, bool SPLIT = false>
-__device__ __forceinline__ ChainHead walk_record_levels(const DevTrie &t, const int4 &rec, int nlev, float *ls,
-                                                        int *ln, int lane, int wave = 0,
-                                                        const float *pf_src = nullptr, float *pf_dst = nullptr,
-                                                        int pf_n = 0) {
+// of W (SPLIT: each wavefront owns exactly one stripe, and loads only its part
+// of each level).  When pf_src is given, pf_n words from it are also copied
+// into pf_dst (the owned stripes) once the record is in (a prefetch that
+// rides along with the dense row and the arcs).  DENSE_ISSUED: the caller
+// already issued the copy of the dense row (before any arc load, which orders
+// the arcs' LDS writes after it).
+template <int W = 1, bool SPLIT = false, bool DENSE_ISSUED = false>
+__device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
+                                                 int lane, int wave = 0, const float *pf_src = nullptr,
+                                                 float *pf_dst = nullptr, int pf_n = 0) {
     const ChainHead h = head_of(rec);
-    dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
+    if (!DENSE_ISSUED) dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
     if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
     for (int j = nlev; j >= 1; --j) {
         int a0, end;
@@ -349,6 +232,10 @@ __device__ __forceinline__ ChainHead walk_record_levels(const DevTrie &t, const 
                 const int a = a0 + u * kWave + lane;
                 if (a < end) r[u] = t.arcs[a];
             }
+            // one wait the compiler sees for all four loads: otherwise, since
+            // the writes below may be skipped, it keeps them pending across
+            // the loop and waits before each load of the next chunk
+            wait_loads();
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int a = a0 + u * kWave + lane;
@@ -359,39 +246,6 @@ __device__ __forceinline__ ChainHead walk_record_levels(const DevTrie &t, const 
             }
         }
     }
-    wait_lds_copies();
-    return h;
-}
-
-template <int W = 1, bool DENSE_ISSUED = false, int UMAX = kArcSlots, bool SPLIT = false>
-__device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
-                                                 int lane, int wave = 0, const float *pf_src = nullptr,
-                                                 float *pf_dst = nullptr, int pf_n = 0) {
-    static_assert(UMAX == 4 || UMAX == 8 || UMAX == 16, "stripe slots per pass");
-    const ChainHead h = head_of(rec);
-    const int q = chain_stripes<W, SPLIT>(rec, nlev, wave);
-    LevelCursor c = cursor_start<W, SPLIT>(rec, nlev, wave);
-    if (q == 0) {
-        if (!DENSE_ISSUED) dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
-        if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
-    } else if (q <= 2) {
-        walk_first_pass<W, SPLIT, 2, DENSE_ISSUED>(t, rec, c, h.dense_row, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
-    } else if (q <= 4 || UMAX == 4) {
-        walk_first_pass<W, SPLIT, 4, DENSE_ISSUED>(t, rec, c, h.dense_row, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
-    } else if (q <= 8 || UMAX == 8) {
-        walk_first_pass<W, SPLIT, 8, DENSE_ISSUED>(t, rec, c, h.dense_row, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
-    } else {
-        walk_first_pass<W, SPLIT, UMAX, DENSE_ISSUED>(t, rec, c, h.dense_row, ls, ln, lane, wave, pf_src, pf_dst, pf_n);
-    }
-    while (c.j >= 1) {   // chains longer than one pass: UMAX stripes per further round trip
-        ArcPass<UMAX> p;
-        issue_pass<W, SPLIT, UMAX>(t, rec, c, lane, wave, p);
-        wait_lds_copies();
-        write_pass<W, UMAX>(p, ls, ln, wave);
-    }
-    // Every copy into LDS has landed from here on.  Waiting once here also keeps
-    // the readers' loops free of waits: on gfx950 stores count in vmcnt too, so
-    // a wait inside a loop that also stores would drain those stores each turn.
     wait_lds_copies();
     return h;
 }
@@ -411,7 +265,7 @@ __device__ __forceinline__ ChainHead walk_into_lds_dense_first(const DevTrie &t,
     dense_to_lds(t, dense_row, ls, ln, lane);
     int nlev;
     const int4 rec = fetch_record(t, s, lane, nlev);
-    return walk_record<1, true>(t, rec, nlev, ls, ln, lane);
+    return walk_record<1, false, true>(t, rec, nlev, ls, ln, lane);
 }
 
 // Final (score, next state) of one LDS slot.

@@ -22,7 +22,7 @@ second over the timed steps.  The same run also reports:
 * the same decode at B = 4096 utterances x 200 frames, with its algorithmic
   HBM bytes (ASR rows, and chain records and arcs on the frames that consult
   the LM);
-* the k best fused tokens (beam expansion) of 1024 hypotheses, k = 4 and 32;
+* the k best fused tokens (beam expansion) of 1024 hypotheses, k = 4, 32 and 128;
 * plain fusion on the 200k-n-gram 4-gram at B = 32 hypotheses x 200 steps;
 * cpu_baseline: the CPU oracle on a bounded sample of the same workload, on all
   host cores; cpu_baseline_decode: the oracle on the whole CTC decode above,
@@ -396,7 +396,7 @@ def main():
     gk.manual_seed(seed_for("ctc_b256_t1000") + 10)
     kasr = torch.log_softmax(torch.randn((Bk, V), generator=gk, device=dev) * 3.0, dim=-1)
     topk = {"workload": f"{Bk} hypotheses (256 utterances x beam 4), V={V}, 20M 6-gram, lambda={fspec.lam}"}
-    for kk in (4, 32):
+    for kk in (4, 32, 128):
         ktok = torch.empty((Bk, kk), dtype=torch.int32, device=dev)
         ksc = torch.empty((Bk, kk), dtype=torch.float32, device=dev)
         knx = torch.empty((Bk, kk), dtype=torch.int32, device=dev)
@@ -411,7 +411,7 @@ def main():
         topk[f"k{kk}_us_per_call"] = f0.elapsed_time(f1) * 1e3 / 50
     assert lm.check_states() == 0
     log(f"fused top-k over {Bk} hypotheses: k=4 {topk['k4_us_per_call']:.1f} us, "
-        f"k=32 {topk['k32_us_per_call']:.1f} us per call")
+        f"k=32 {topk['k32_us_per_call']:.1f} us, k=128 {topk['k128_us_per_call']:.1f} us per call")
     del kasr
 
     # ---- plain fusion on the 200k 4-gram: B = 32 hypotheses x 200 steps

@@ -771,6 +771,56 @@ def test_fused_topk_vocab_sizes(dev, V):
         assert np.array_equal(np.isfinite(g), fin) and np.abs(g[fin] - osc[fin]).max() <= TOL
 
 
+@pytest.mark.parametrize("k", [8, 100, 256])
+def test_fused_topk_large_k(dev, k):
+    """The threshold selection (k >= 8): rows of full ties, -inf rows, rows with
+    fewer finite tokens than k, rows whose fused values are coarsely quantised
+    so that many tokens tie across lanes and stripes, and ordinary rows."""
+    m, lm, o = model_pair("fourgram_200k")
+    V = m.vocab_size
+    B = 24
+    states = uniform_states(m, B, seed=70 + k)
+    asr = asr_logprobs((B, V), seed=71 + k)
+    asr[0] = -3.0
+    asr[1] = -np.inf
+    asr[2] = -np.inf
+    asr[2, ::11] = -1.0                       # 94 finite tokens
+    asr[3:8] = np.round(asr[3:8] * 2) / 2     # many exact ties at lambda = 0
+    for lam in (0.0, 0.6):
+        case(f"fused top-k large k={k} lambda={lam}")
+        tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), lam, k, torch.from_numpy(states).to(dev))
+        torch.cuda.synchronize()
+        assert lm.check_states() == 0
+        ot, osc, onx = o.fused_topk(asr, lam, k, states)
+        assert np.array_equal(tok.cpu().numpy(), ot)
+        assert np.array_equal(nx.cpu().numpy(), onx)
+        g = sc.cpu().numpy()
+        fin = np.isfinite(osc)
+        assert np.array_equal(np.isfinite(g), fin) and np.abs(g[fin] - osc[fin]).max() <= TOL
+        assert ot[0].tolist() == list(range(k)) or lam != 0.0
+
+
+def test_fused_topk_k_equals_vocab(dev):
+    """k = V on a V = 128 model: every token once, in the definition's order."""
+    m, lm, o = model_pair("trigram_v128")
+    V = m.vocab_size
+    B = 16
+    states = uniform_states(m, B, seed=81)
+    asr = asr_logprobs((B, V), seed=82)
+    asr[0] = -2.0
+    asr[1, :] = -np.inf
+    asr[1, 5::9] = 0.0
+    case(f"fused top-k k=V={V}")
+    tok, sc, nx = lm.fused_topk(torch.from_numpy(asr).to(dev), 0.4, V, torch.from_numpy(states).to(dev))
+    torch.cuda.synchronize()
+    ot, osc, onx = o.fused_topk(asr, 0.4, V, states)
+    assert np.array_equal(tok.cpu().numpy(), ot) and np.array_equal(nx.cpu().numpy(), onx)
+    assert (np.sort(tok.cpu().numpy(), axis=1) == np.arange(V)).all()
+    g = sc.cpu().numpy()
+    fin = np.isfinite(osc)
+    assert np.array_equal(np.isfinite(g), fin) and np.abs(g[fin] - osc[fin]).max() <= TOL
+
+
 def test_fused_topk_odd_vocab_and_bad_state(dev):
     m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
     V = m.vocab_size

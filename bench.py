@@ -271,22 +271,23 @@ def main():
     log(f"fused CTC: {fused['us_per_step']:.1f} us/step, {fused['frames_per_s']:.3g} frames/s")
 
     # ---- transducer mode, one launch per step (the LM consulted on non-blank frames), B = 32 and 256
+    Tt = min(T, 200)
     transducer = {"workload": f"transducer, 20M 6-gram, {V + 1} classes (log_softmax of N(0,3) logits, blank +"
-                              f"{fspec.blank_boost}), lambda={fspec.lam}, one launch per step, 200 steps"}
+                              f"{fspec.blank_boost}), lambda={fspec.lam}, one launch per step, {Tt} steps"}
     for Bt in (32, 256):
         tst = torch.zeros(Bt, dtype=torch.int32, device=dev)
-        ttok = torch.empty((200, Bt), dtype=torch.int32, device=dev)
-        trows = [asr[t, :Bt] for t in range(200)]
-        for t in range(20):
+        ttok = torch.empty((Tt, Bt), dtype=torch.int32, device=dev)
+        trows = [asr[t, :Bt] for t in range(Tt)]
+        for t in range(min(20, Tt)):
             lm.fused_greedy_step(trows[t], fspec.lam, tst, mode=ng.NGPU_FUSION_TRANSDUCER, tokens=ttok[t])
         tst.zero_()
         torch.cuda.synchronize()
         f0.record(stream)
-        for t in range(200):
+        for t in range(Tt):
             lm.fused_greedy_step(trows[t], fspec.lam, tst, mode=ng.NGPU_FUSION_TRANSDUCER, tokens=ttok[t])
         f1.record(stream)
         torch.cuda.synchronize()
-        transducer[f"b{Bt}_us_per_step"] = f0.elapsed_time(f1) * 1e3 / 200
+        transducer[f"b{Bt}_us_per_step"] = f0.elapsed_time(f1) * 1e3 / Tt
         transducer[f"b{Bt}_lm_share"] = float((ttok != V).float().mean())
     assert lm.check_states() == 0
     log(f"fused transducer: {transducer['b32_us_per_step']:.1f} us/step at B=32, "

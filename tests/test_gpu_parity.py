@@ -771,6 +771,22 @@ def test_fused_topk_vocab_sizes(dev, V):
         assert np.array_equal(np.isfinite(g), fin) and np.abs(g[fin] - osc[fin]).max() <= TOL
 
 
+def test_sync_check(dev):
+    """ngpu_lm_sync_check: NGPU_E_BAD_STATE after queries that met out-of-range
+    states (the count clears), NGPU_OK after clean ones."""
+    m, lm, o = model_pair("trigram_v128")
+    states = uniform_states(m, 12, seed=90)
+    states[[2, 7]] = [-1, m.num_states]
+    case("sync check")
+    run_advance(lm, states, dev)
+    with pytest.raises(ng.NgpuError) as e:
+        lm.sync_check()
+    assert e.value.code == -12
+    lm.sync_check()                      # cleared
+    run_advance(lm, uniform_states(m, 12, seed=91), dev)
+    lm.sync_check()
+
+
 @pytest.mark.parametrize("k", [8, 100, 256])
 def test_fused_topk_large_k(dev, k):
     """The threshold selection (k >= 8): rows of full ties, -inf rows, rows with

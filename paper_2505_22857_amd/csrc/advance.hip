@@ -60,6 +60,10 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
             dense_l = hd.dense_row;   // lets the walk start the dense-row copy before the record load
         }
     }
+    // The scan's loads are complete here; otherwise the wait for them stays at
+    // the head of the loop below, where it would also drain the previous
+    // hypothesis's stores before the next one's loads are issued.
+    wait_loads();
     uint64_t todo = __ballot(mine);
     while (todo) {
         const int i = __builtin_ctzll(todo);
@@ -103,6 +107,82 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
                 slot_value(h, ls[v], ln[v], x, n);
                 __builtin_nontemporal_store(x, orow + v);
                 __builtin_nontemporal_store(n, nrow + v);
+            }
+        }
+    }
+}
+
+// The XCD-grouped mapping with two wavefronts per hypothesis, independent of
+// each other: part p walks and writes tokens [512 p, 512 p + 512) through its
+// own 4 KiB LDS row, loading only its half of every level (the split counts:
+// arcs are sorted by token).  Half the LDS per wavefront lets more of them,
+// and their stores, be in flight per CU.  V in (768, 1024], a multiple of 4.
+template <int G>
+__global__ __launch_bounds__(kWave) void advance_half_kernel(DevTrie t, const int32_t *__restrict__ states, int64_t B,
+                                                             float *__restrict__ scores,
+                                                             int32_t *__restrict__ next) {
+    extern __shared__ float lds[];
+    const int lane = threadIdx.x;
+    const int grp = int(blockIdx.x % G);
+    const int part = int((blockIdx.x / G) & 1);
+    const int64_t base = int64_t(blockIdx.x / (2 * G)) * G;
+    if (base >= B) return;
+    const int V = t.vocab_size;
+    const int c0 = 2 * kStripe * part;   // slot of token v: v - c0
+    float *ls = lds;
+    int *ln = reinterpret_cast<int *>(lds + 2 * kStripe);
+
+    int s_l = -1, dense_l = -1;
+    bool mine = false;
+    const int64_t bl = base + lane;
+    if (lane < G && bl < B) {
+        s_l = states[bl];
+        if (s_l < 0 || s_l >= t.num_states) {
+            s_l = -1;
+            mine = (bl % G) == grp;
+        } else {
+            int nl;
+            const ChainHead hd = *reinterpret_cast<const ChainHead *>(chain_record(t, s_l, nl));
+            mine = chain_group(hd) == grp;
+            dense_l = hd.dense_row;
+        }
+    }
+    wait_loads();   // as in advance_kernel
+    uint64_t todo = __ballot(mine);
+    while (todo) {
+        const int i = __builtin_ctzll(todo);
+        todo &= todo - 1;
+        const int64_t b = base + i;
+        float *orow = scores + b * V;
+        int32_t *nrow = next + b * V;
+        const int s = __builtin_amdgcn_readlane(s_l, i);
+        if (s < 0) {
+            if (lane == 0 && part == 0) atomicAdd(&t.status[0], 1);
+            for (int v = c0 + lane; v < V && v < c0 + 2 * kStripe; v += kWave) {
+                orow[v] = NAN;
+                nrow[v] = -1;
+            }
+            continue;
+        }
+        dense_half_to_lds(t, __builtin_amdgcn_readlane(dense_l, i), ls, ln, part, lane);
+        int nlev;
+        const int4 rec = fetch_record(t, s, lane, nlev);
+        const ChainHead h = walk_record<1, false, true, true>(t, rec, nlev, ls, ln, lane, part);
+        for (int c = c0; c < V && c < c0 + 2 * kStripe; c += kStripe) {
+            const int v = c + 4 * lane;
+            if (v < V) {
+                const int4 n4 = *reinterpret_cast<const int4 *>(ln + (v - c0));
+                const float4 x4 = *reinterpret_cast<const float4 *>(ls + (v - c0));
+                nf4 xo;
+                ni4 no;
+                float x;
+                int n;
+                slot_value(h, x4.x, n4.x, x, n); xo.x = x; no.x = n;
+                slot_value(h, x4.y, n4.y, x, n); xo.y = x; no.y = n;
+                slot_value(h, x4.z, n4.z, x, n); xo.z = x; no.z = n;
+                slot_value(h, x4.w, n4.w, x, n); xo.w = x; no.w = n;
+                __builtin_nontemporal_store(xo, reinterpret_cast<nf4 *>(orow + v));
+                __builtin_nontemporal_store(no, reinterpret_cast<ni4 *>(nrow + v));
             }
         }
     }
@@ -217,6 +297,7 @@ static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B,
 //    9.4 us at 128 hypotheses, 9.0 against 9.9 at 512, 9.6 against 10.0 at
 //    1024; 10.7 against 10.5 at 1536 and 12.1 against 11.2 at 2048.
 constexpr int64_t kStripedMaxBatch = 1024;
+constexpr bool kAdvanceHalves = true;
 constexpr int64_t kGroupedMinBatch = 20480;
 constexpr int kHpbGrouped = 1;
 constexpr int kHpbPlain = 2;
@@ -233,7 +314,16 @@ hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, fl
                           hipStream_t stream) {
     const bool vec = (t.vocab_size % 4 == 0) && (reinterpret_cast<uintptr_t>(scores) % 16 == 0) &&
                      (reinterpret_cast<uintptr_t>(next) % 16 == 0);
-    if (B >= kGroupedMinBatch) return launch_hpb<kHpbGrouped, kGroups>(t, states, B, scores, next, stream, vec);
+    if (B >= kGroupedMinBatch) {
+        const int64_t chunks = (B + kGroups - 1) / kGroups;
+        if (vec && kAdvanceHalves && (t.vocab_size + kStripe - 1) / kStripe == 4 &&
+            2 * chunks * kGroups * kWave <= int64_t(UINT32_MAX)) {   // dispatch size in work-items
+            hipLaunchKernelGGL(advance_half_kernel<kGroups>, dim3(unsigned(2 * chunks * kGroups)), dim3(kWave),
+                               size_t(4 * kStripe) * sizeof(float), stream, t, states, B, scores, next);
+            return hipGetLastError();
+        }
+        return launch_hpb<kHpbGrouped, kGroups>(t, states, B, scores, next, stream, vec);
+    }
     if (B <= kStripedMaxBatch) {   // wavefronts per hypothesis: one per stripe, at most four
         const int stripes = (t.vocab_size + kStripe - 1) / kStripe;
         if (stripes >= 4) return launch_striped<4>(t, states, B, scores, next, stream, vec);

@@ -642,12 +642,66 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
     }
 }
 
+// Inclusive prefix sum over the lanes of a wave (the DPP pattern of
+// wave_max_u32 with additions).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ unsigned add_step(unsigned x) {
+    return x + unsigned(__builtin_amdgcn_update_dpp(0, int(x), CTRL, ROW_MASK, 0xf, true));
+}
+
+__device__ __forceinline__ unsigned wave_incl_sum(unsigned x) {
+    x = add_step<0x111, 0xf>(x);
+    x = add_step<0x112, 0xf>(x);
+    x = add_step<0x114, 0xf>(x);
+    x = add_step<0x118, 0xf>(x);
+    x = add_step<0x142, 0xa>(x);
+    x = add_step<0x143, 0xc>(x);
+    return x;
+}
+
+__device__ __forceinline__ unsigned wave_sum(unsigned x) {
+    return unsigned(__builtin_amdgcn_readlane(int(wave_incl_sum(x)), kWave - 1));
+}
+
+// The k (distinct) sort keys in sk[0, k), with their scores and next states,
+// written out in descending key order: lane l ranks entries l + 64 r (r < NR,
+// k <= 64 NR) by counting the keys above them.
+template <int NR>
+__device__ __forceinline__ void rank_and_store(const unsigned long long *sk, const float *ssc, const int *snx, int k,
+                                               int lane, int32_t *otok, float *osc, int32_t *onx) {
+    unsigned long long mine[NR];
+    int rank[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        mine[r] = lane + r * kWave < k ? sk[lane + r * kWave] : ~0ull;
+        rank[r] = 0;
+    }
+#pragma unroll 8
+    for (int q = 0; q < k; ++q) {
+        const unsigned long long o = sk[q];
+#pragma unroll
+        for (int r = 0; r < NR; ++r) rank[r] += o > mine[r] ? 1 : 0;
+    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int e = lane + r * kWave;
+        if (e < k) {
+            otok[rank[r]] = int(~unsigned(mine[r] & 0xffffffffu));
+            osc[rank[r]] = ssc[e];
+            onx[rank[r]] = snx[e];
+        }
+    }
+}
+
 // The same selection in a number of steps that does not grow with k (V <=
 // 256 * SPL): keys are the order-preserving images of the fused values
 // (value_key; tokens past V get 0, below every token's key).
-//   1. the threshold T, the largest key with at least k keys >= T, by a binary
-//      search over its 32 bits; a count of keys >= a candidate is one ballot
-//      and one scalar popcount per register slot, no cross-lane reduction;
+//   1. the threshold T, the largest key with at least k keys >= T (the k-th
+//      largest key), by a binary search over its bits: a count of the keys
+//      >= a candidate is a compare and add per register slot and one wave sum
+//      (DPP).  The bits that a lower bound of T and the largest key share are
+//      T's from the start, and the search stops as soon as a candidate has
+//      exactly k keys >= it: then those are the k taken and no tie is cut;
 //   2. every key above T is taken, and of the keys equal to T the lowest
 //      token indices until k are taken (a token's rank among them from
 //      ballots and lane-prefix counts: token 256 c + 4 l + j sits in slot
@@ -705,44 +759,77 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
             key[4 * c + j] = v0 + j < V ? value_key(f[4 * c + j]) : 0u;
         }
     }
-    // 1. threshold; the search stops early when exactly k keys are >= T (then
-    // those are the k taken and no tie is cut)
-    unsigned T = 0;
-    bool exact = false;
-    for (int bit = 31; bit >= 0 && !exact; --bit) {
-        const unsigned cand = T | (1u << bit);
-        int cnt = 0;
+    // 1. the threshold T.  It lies between a lower bound lo (for k <= 64 j,
+    // the smallest over the lanes of a lane's j-th largest key: at least
+    // 64 j >= k keys are >= it; 0 for k > 128) and the largest key, so the
+    // bits above the highest one in which those two differ are T's already.
+    unsigned lo = 0, mx = 0;
+    if (k <= 2 * kWave) {
+        unsigned m1 = 0, m2 = 0;   // the lane's largest and second largest key
 #pragma unroll
-        for (int i = 0; i < kN; ++i) cnt += __builtin_popcountll(__ballot(key[i] >= cand));
+        for (int i = 0; i < kN; ++i) {
+            m2 = max(m2, min(m1, key[i]));
+            m1 = max(m1, key[i]);
+        }
+        mx = wave_max_u32(m1);
+        lo = ~wave_max_u32(~(k <= kWave ? m1 : m2));
+    } else {
+        unsigned m1 = 0;
+#pragma unroll
+        for (int i = 0; i < kN; ++i) m1 = max(m1, key[i]);
+        mx = wave_max_u32(m1);
+    }
+    const unsigned diff = lo ^ mx;
+    const int top = diff ? 31 - __builtin_clz(diff) : -1;
+    unsigned T = top < 0 ? mx : mx & ~((2u << top) - 1u);   // top = 31: no bit known (2u << 31 is 0)
+    bool exact = false;   // the keys >= T number exactly k
+    for (int bit = top; bit >= 0 && !exact; --bit) {
+        const unsigned cand = T | (1u << bit);
+        unsigned c = 0;
+#pragma unroll
+        for (int i = 0; i < kN; ++i) c += key[i] >= cand ? 1u : 0u;
+        const int cnt = int(wave_sum(c));
         if (cnt >= k) T = cand;
         exact = cnt == k;
     }
-    // 2. taken entries
-    int above = 0;
+    int above = k;
+    if (!exact) {   // T is the k-th key itself: count the keys above it
+        unsigned c = 0;
 #pragma unroll
-    for (int i = 0; i < kN; ++i) above += __builtin_popcountll(__ballot(exact ? key[i] >= T : key[i] > T));
-    const int ties_needed = k - above;   // 0 when exact
+        for (int i = 0; i < kN; ++i) c += key[i] > T ? 1u : 0u;
+        above = int(wave_sum(c));
+    }
+    // 2. taken entries: every key >= T when exact; otherwise T is the k-th
+    // key itself, `above` keys exceed it, and of the keys equal to it the
+    // lowest token indices are taken
     bool take[kN];
-    int ties_before = 0;   // ties at T in earlier stripes (uniform)
+    if (exact) {
 #pragma unroll
-    for (int c = 0; c < SPL; ++c) {
-        unsigned long long m[4];
-        int below = 0;      // ties of this stripe in lower lanes
+        for (int i = 0; i < kN; ++i) take[i] = key[i] >= T;
+    } else {
+        const int ties_needed = k - above;
+        int ties_before = 0;   // ties at T in earlier stripes (uniform)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            m[j] = __ballot(key[4 * c + j] == T);
-            below += int(__builtin_amdgcn_mbcnt_hi(unsigned(m[j] >> 32), __builtin_amdgcn_mbcnt_lo(unsigned(m[j]), 0u)));
+        for (int c = 0; c < SPL; ++c) {
+            unsigned long long m[4];
+            int below = 0;      // ties of this stripe in lower lanes
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                m[j] = __ballot(key[4 * c + j] == T);
+                below += int(__builtin_amdgcn_mbcnt_hi(unsigned(m[j] >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo(unsigned(m[j]), 0u)));
+            }
+            int own = 0;        // ties of this lane in earlier slots of the stripe
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int i = 4 * c + j;
+                const bool tie = key[i] == T;
+                take[i] = key[i] > T || (tie && ties_before + below + own < ties_needed);
+                own += tie ? 1 : 0;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) ties_before += __builtin_popcountll(m[j]);
         }
-        int own = 0;        // ties of this lane in earlier slots of the stripe
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int i = 4 * c + j;
-            const bool tie = key[i] == T;
-            take[i] = exact ? key[i] >= T : (key[i] > T || (tie && ties_before + below + own < ties_needed));
-            own += tie ? 1 : 0;
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) ties_before += __builtin_popcountll(m[j]);
     }
     // 3. compaction into LDS (the walked row is in registers now), then ranks
     unsigned long long *sk = reinterpret_cast<unsigned long long *>(lds);
@@ -761,26 +848,12 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
         }
         base += __builtin_popcountll(m);
     }
-    // lane l ranks entries l, l + 64, l + 128, l + 192 (k <= 256)
-    unsigned long long mine[4];
-    int rank[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int r = 0; r < 4; ++r) mine[r] = lane + r * kWave < k ? sk[lane + r * kWave] : ~0ull;
-#pragma unroll 8
-    for (int q = 0; q < k; ++q) {
-        const unsigned long long o = sk[q];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) rank[r] += o > mine[r] ? 1 : 0;
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int e = lane + r * kWave;
-        if (e < k) {
-            otok[rank[r]] = int(~unsigned(mine[r] & 0xffffffffu));
-            osc[rank[r]] = ssc[e];
-            onx[rank[r]] = snx[e];
-        }
-    }
+    if (k <= kWave)
+        rank_and_store<1>(sk, ssc, snx, k, lane, otok, osc, onx);
+    else if (k <= 2 * kWave)
+        rank_and_store<2>(sk, ssc, snx, k, lane, otok, osc, onx);
+    else
+        rank_and_store<4>(sk, ssc, snx, k, lane, otok, osc, onx);
 }
 
 __global__ __launch_bounds__(256) void final_weights_kernel(DevTrie t, const int32_t *__restrict__ states, int64_t B,
@@ -804,8 +877,9 @@ hipError_t launch_final_weights(const DevTrie &t, const int32_t *states, int64_t
 
 // From this k on, the threshold selection beats one reduction per selected
 // token (register layouts, V <= 1024; 1024 hypotheses of the 20M 6-gram:
-// 11.2 against 12.6 us at k = 8, 15.1 against 13.4 at k = 16).
-constexpr int kTopkSelectMinK = 12;
+// 10.3 against 10.7 us at k = 6, 10.6 against 11.4 at k = 8; 10.9 against
+// 10.7 at k = 4).
+constexpr int kTopkSelectMinK = 6;
 
 hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
                              const int32_t *states, int32_t *tokens, float *scores, int32_t *next,

@@ -145,11 +145,17 @@ __device__ __forceinline__ bool owns_token(int tok, int wave) {
 // Arc range of record entry j for wavefront `wave` of W: the whole level, or,
 // when SPLIT (the wavefronts own one 256-token stripe each), the part of it
 // whose tokens fall in the wavefront's stripe, from the level's split counts.
-template <int W, bool SPLIT>
+template <int W, bool SPLIT, bool HALVES = false>
 __device__ __forceinline__ void level_bounds(const int4 &rec, int j, int wave, int &a0, int &end) {
     a0 = __builtin_amdgcn_readlane(rec.x, j);
     end = __builtin_amdgcn_readlane(rec.y, j);
-    if (SPLIT && W > 1) {
+    if (HALVES) {   // wavefront `wave` owns tokens [512 wave, 512 wave + 512)
+        const int c2 = int((unsigned(__builtin_amdgcn_readlane(rec.w, j)) >> 9) & 0x3ffu);
+        if (wave == 0)
+            end = a0 + c2;
+        else
+            a0 += c2;
+    } else if (SPLIT && W > 1) {
         const unsigned sp = unsigned(__builtin_amdgcn_readlane(rec.w, j));
         const int n = end - a0;
         const int c1 = int(sp & 0x1ffu), c2 = int((sp >> 9) & 0x3ffu), c3 = int((sp >> 19) & 0x3ffu);
@@ -185,6 +191,21 @@ __device__ __forceinline__ void copy_stripes_dword(const void *src, void *dst, i
         copy_to_lds_dword(s + c, d + c, n - c < kStripe ? n - c : kStripe, lane);
 }
 
+// Tokens [512 part, 512 part + 512) of dense row `row` into (ls, ln), which
+// hold that half only (slot = token - 512 part; V a multiple of 4).
+__device__ __forceinline__ void dense_half_to_lds(const DevTrie &t, int row, float *ls, int *ln, int part,
+                                                  int lane) {
+    const int V = t.vocab_size;
+    const float *dw = t.dense_w + size_t(row) * V;
+    const int32_t *dt = t.dense_to + size_t(row) * V;
+    const int c0 = 2 * kStripe * part;
+    for (int c = c0; c < V && c < c0 + 2 * kStripe; c += kStripe) {
+        const int n = V - c < kStripe ? V - c : kStripe;
+        copy_to_lds_x4(dw + c, ls + (c - c0), n, lane);
+        copy_to_lds_x4(dt + c, ln + (c - c0), n, lane);
+    }
+}
+
 template <int W>
 __device__ __forceinline__ void dense_stripes_to_lds(const DevTrie &t, int row, float *ls, int *ln, int wave,
                                                      int lane) {
@@ -214,16 +235,21 @@ __device__ __forceinline__ void dense_stripes_to_lds(const DevTrie &t, int row, 
 // rides along with the dense row and the arcs).  DENSE_ISSUED: the caller
 // already issued the copy of the dense row (before any arc load, which orders
 // the arcs' LDS writes after it).
-template <int W = 1, bool SPLIT = false, bool DENSE_ISSUED = false>
+template <int W = 1, bool SPLIT = false, bool DENSE_ISSUED = false, bool HALVES = false>
 __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
                                                  int lane, int wave = 0, const float *pf_src = nullptr,
                                                  float *pf_dst = nullptr, int pf_n = 0) {
     const ChainHead h = head_of(rec);
-    if (!DENSE_ISSUED) dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
+    if (!DENSE_ISSUED) {
+        if (HALVES)
+            dense_half_to_lds(t, h.dense_row, ls, ln, wave, lane);
+        else
+            dense_stripes_to_lds<W>(t, h.dense_row, ls, ln, wave, lane);
+    }
     if (pf_src) copy_stripes_dword<W>(pf_src, pf_dst, pf_n, wave, lane);
     for (int j = nlev; j >= 1; --j) {
         int a0, end;
-        level_bounds<W, SPLIT>(rec, j, wave, a0, end);
+        level_bounds<W, SPLIT, HALVES>(rec, j, wave, a0, end);
         const float acc = __int_as_float(__builtin_amdgcn_readlane(rec.z, j));
         for (; a0 < end; a0 += 4 * kWave) {
             Arc r[4];
@@ -239,9 +265,10 @@ __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &r
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int a = a0 + u * kWave + lane;
-                if (a < end && owns_token<W>(r[u].tok, wave)) {
-                    ls[r[u].tok] = acc + r[u].w;
-                    ln[r[u].tok] = r[u].to | kFinal;
+                if (a < end && (HALVES || owns_token<W>(r[u].tok, wave))) {
+                    const int slot = HALVES ? r[u].tok - 2 * kStripe * wave : r[u].tok;
+                    ls[slot] = acc + r[u].w;
+                    ln[slot] = r[u].to | kFinal;
                 }
             }
         }
@@ -357,5 +384,6 @@ __device__ __forceinline__ int wave_argmax(float bx, int bi, float &best) {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 }  // namespace ngpu

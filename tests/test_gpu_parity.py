@@ -155,15 +155,20 @@ def test_advance_6gram_20m_bench_launch_sampled(dev):
     assert int(nx.min()) >= 0 and int(nx.max()) < m.num_states
 
 
-@pytest.mark.parametrize("which", ["4gram_200k", "V1025", "N10"])
+@pytest.mark.parametrize("which", ["4gram_200k", "V800", "V1025", "N10"])
 def test_advance_grouped_mapping_with_bad_states(dev, which):
     """Batches of 20480 and more take the XCD-grouped mapping: every row, including
     rows of out-of-range states (written by exactly one owner), vs the oracle.
+    V in (768, 1024] runs it with two wavefronts per hypothesis, one per
+    512-token half (V = 800: a ragged second half); V = 1025 with one.
     N10: a 10-gram, whose order-9 states have chain records longer than the
     scan preloads."""
     if which == "4gram_200k":
         m, lm, o = model_pair("fourgram_200k")
         B = 40000
+    elif which == "V800":
+        m, lm, o = pair("V800N4", lambda: generate_model(800, [800, 4800, 4800, 4800], 1.0, seed=804))
+        B = 20488
     elif which == "V1025":
         m, lm, o = pair("V1025N4", lambda: generate_model(1025, [1025, 6150, 6150, 6150], 1.0, seed=1029))
         B = 20481
@@ -787,11 +792,13 @@ def test_sync_check(dev):
     lm.sync_check()
 
 
-@pytest.mark.parametrize("k", [8, 100, 256])
+@pytest.mark.parametrize("k", [6, 8, 64, 100, 128, 256])
 def test_fused_topk_large_k(dev, k):
-    """The threshold selection (k >= 8): rows of full ties, -inf rows, rows with
+    """The threshold selection (k >= 6): rows of full ties, -inf rows, rows with
     fewer finite tokens than k, rows whose fused values are coarsely quantised
-    so that many tokens tie across lanes and stripes, and ordinary rows."""
+    so that many tokens tie across lanes and stripes, and ordinary rows.  k =
+    64 and 128 are the largest k whose search starts from the smallest lane
+    maximum and lane second-maximum; above 128 it starts from no lower bound."""
     m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B = 24

@@ -197,6 +197,8 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
                                                                      int64_t B, float *__restrict__ scores,
                                                                      int32_t *__restrict__ next) {
     extern __shared__ float lds[];
+    load_trie_args(t);
+    load_args(states, B, scores, next);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
     const int64_t b = blockIdx.x;
@@ -216,7 +218,7 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
         return;
     }
     int nlev;
-    const int4 rec = fetch_record(t, s, lane, nlev);
+    const int4 rec = fetch_record<true>(t, s, lane, nlev);
     const ChainHead h = walk_record<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave);
     for (int c = kStripe * wave; c < V; c += kStripe * W) {
         if (VEC) {

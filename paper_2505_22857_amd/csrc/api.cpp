@@ -60,6 +60,9 @@ ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     t.dense_w = reinterpret_cast<const float *>(base + h.off_dense_w);
     t.dense_to = reinterpret_cast<const int32_t *>(base + h.off_dense_to);
     t.arcs = reinterpret_cast<const ngpu::Arc *>(base + h.off_arcs);
+    t.top_arcs = reinterpret_cast<const ngpu::TopArc *>(base + h.off_top_arcs);
+    t.top_begin = int32_t(h.top_arc_begin);
+    t.to_delta = h.arc_to_delta;
     t.final_w = h.has_final ? reinterpret_cast<const float *>(base + h.off_final) : nullptr;
     t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + h.off_status);
     t.num_states = int32_t(lm->S);

@@ -236,7 +236,8 @@ __device__ __forceinline__ int first_token_state(const ChainHead &h, const float
 // previous label (CTC).  after_record runs once the chain record's load is
 // issued.  Returns the label and updates s; all lanes of all W wavefronts
 // return the same values.
-template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook, bool SPLIT = false>
+template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook, bool SPLIT = false,
+          bool SGPR_TABLES = false>
 __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, float rowV, float lambda, int &s,
                                            int pv, float *ls, int *ln, Exchange *xc, int &xi, int wave, int lane,
                                            const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0,
@@ -246,7 +247,7 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, flo
     // The chain record is fetched first: in CTC and transducer modes its load
     // overlaps the plain ASR argmax, which may still find that the LM is not needed.
     int nlev;
-    const int4 rec = fetch_record(t, s, lane, nlev);
+    const int4 rec = fetch_record<SGPR_TABLES>(t, s, lane, nlev);
     after_record();
     if (MODE == kCtc || MODE == kTransducer) {
         if (ROW_PENDING) wait_lds_copies();
@@ -302,6 +303,8 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
                                                                 int32_t *__restrict__ prev,
                                                                 int32_t *__restrict__ tokens) {
     extern __shared__ float lds[];
+    load_trie_args(t);
+    load_args(asr, B, ld, lambda, states, prev, tokens);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
     const int64_t b = blockIdx.x;
@@ -312,13 +315,16 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     float *arow = reinterpret_cast<float *>(ln + lds_row(V));
     Exchange *xc = reinterpret_cast<Exchange *>(arow + asr_row_words(V));
 
-    // the ASR row's copy into LDS goes out with the state load
+    // the state, the previous label and blank's score go out first, then the
+    // ASR row's copy into LDS, so their wait leaves the copy in flight
     const float *src = asr + b * ld;
+    const int s_l = states[b];
+    const int pv_l = MODE == kCtc ? prev[b] : -1;
+    const float rowV_l = MODE == kPlain ? 0.0f : src[V];
     copy_stripes_dword<W>(src, arow, V, wave, lane);
-    const float rowV = MODE == kPlain ? 0.0f : src[V];
-    // the previous label is loaded with the state, not after the state's check
-    const int pv = MODE == kCtc ? __builtin_amdgcn_readfirstlane(prev[b]) : -1;
-    int s = __builtin_amdgcn_readfirstlane(states[b]);
+    int s = __builtin_amdgcn_readfirstlane(s_l);
+    const int pv = __builtin_amdgcn_readfirstlane(pv_l);
+    const float rowV = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, rowV_l)));
     if (s < 0 || s >= t.num_states) {
         if (wave == 0 && lane == 0) {
             atomicAdd(&t.status[0], 1);
@@ -330,7 +336,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     int xi = 0;
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
-    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, SPLIT>(
+    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, SPLIT, true>(
         t, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
     if (wave == 0 && lane == 0) {
         tokens[b] = label;
@@ -471,6 +477,8 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
                                                            int32_t *__restrict__ tokens, float *__restrict__ scores,
                                                            int32_t *__restrict__ next) {
     extern __shared__ float lds[];
+    load_trie_args(t);
+    load_args(asr, B, ld, lambda, k, states, tokens, scores, next);
     const int lane = threadIdx.x;
     const int64_t b = blockIdx.x;
     if (b >= B) return;
@@ -481,8 +489,9 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     int32_t *otok = tokens + b * k;
     float *osc = scores + b * k;
     int32_t *onx = next + b * k;
+    const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
     copy_to_lds_dword(asr + b * ld, arow, V, lane);
-    const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    const int s = __builtin_amdgcn_readfirstlane(s_l);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
         for (int j = lane; j < k; j += kWave) {
@@ -493,7 +502,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds<true>(t, s, ls, ln, lane);   // its final wait covers the ASR row too
     constexpr int kTaken = int32_t(0x80000000u);
     float bx = -__builtin_inff();
     int bi = kNone;
@@ -563,6 +572,8 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
                                                                int32_t *__restrict__ next) {
     static_assert(4 * SPL <= 32, "the taken mask holds 32 tokens per lane");
     extern __shared__ float lds[];
+    load_trie_args(t);
+    load_args(asr, B, ld, lambda, k, states, tokens, scores, next);
     const int lane = threadIdx.x;
     const int64_t b = blockIdx.x;
     if (b >= B) return;
@@ -573,8 +584,9 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
     int32_t *otok = tokens + b * k;
     float *osc = scores + b * k;
     int32_t *onx = next + b * k;
+    const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
     copy_to_lds_dword(asr + b * ld, arow, V, lane);
-    const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    const int s = __builtin_amdgcn_readfirstlane(s_l);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
         for (int j = lane; j < k; j += kWave) {
@@ -585,7 +597,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds<true>(t, s, ls, ln, lane);   // its final wait covers the ASR row too
     // value i = 4 c + j of this lane is token 256 c + 4 lane + j
     float f[4 * SPL];
     int n[4 * SPL];
@@ -718,6 +730,8 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
                                                                   int32_t *__restrict__ next) {
     constexpr int kN = 4 * SPL;
     extern __shared__ float lds[];
+    load_trie_args(t);
+    load_args(asr, B, ld, lambda, k, states, tokens, scores, next);
     const int lane = threadIdx.x;
     const int64_t b = blockIdx.x;
     if (b >= B) return;
@@ -728,8 +742,9 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
     int32_t *otok = tokens + b * k;
     float *osc = scores + b * k;
     int32_t *onx = next + b * k;
+    const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
     copy_to_lds_dword(asr + b * ld, arow, V, lane);
-    const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    const int s = __builtin_amdgcn_readfirstlane(s_l);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
         for (int j = lane; j < k; j += kWave) {
@@ -740,7 +755,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds<true>(t, s, ls, ln, lane);   // its final wait covers the ASR row too
     // slot i = 4 c + j of this lane is token 256 c + 4 lane + j
     float f[kN];
     int n[kN];

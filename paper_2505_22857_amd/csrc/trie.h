@@ -20,10 +20,15 @@
 //            to one of kGroups groups, balanced by the number of states whose
 //            chain ends in it; a query kernel may serve each group from one XCD
 //            so that the group's rows stay in that XCD's L2.
-//   arcs     Arc [A3]    arcs of states of order >= 2 (n-grams of order >= 3),
-//                        sorted by (from_state, token) (Section 2.2); one
-//                        12-byte record {token, weight, next state} per arc,
-//                        so 64 lanes read 64 arcs with one load instruction
+//   arcs     arcs of states of order >= 2 (n-grams of order >= 3), sorted by
+//            (from_state, token) (Section 2.2), numbered 0 .. A3 - 1; 64 lanes
+//            read 64 arcs of a level with one load instruction.  An arc of
+//            order k < N leads to the state of its own n-gram, and states and
+//            arcs of one order share their sorted order, so its next state is
+//            its index plus arc_to_delta (= first[3]):
+//              Arc {token, weight} [top_arc_begin]           orders 3 .. N-1
+//            The arcs of order N lead to their n-gram's suffix and keep it:
+//   top_arcs TopArc {token, weight, next} [A3 - top_arc_begin]   order N
 //   final    float [S]   with </s> in the model: each state's end-of-sentence
 //                        weight, folded through its backoff chain at build
 //                        time (Section 2.3, AED)
@@ -38,7 +43,7 @@
 
 namespace ngpu {
 
-constexpr uint32_t kImageMagic = 0x334d4c4e;  // "NLM3"
+constexpr uint32_t kImageMagic = 0x344d4c4e;  // "NLM4"
 constexpr size_t kAlign = 256;
 constexpr int32_t kDenseBackoff = int32_t(0x80000000u);  // flag bit in dense_to
 constexpr int kGroups = 8;                                // dense-row groups (one per XCD)
@@ -57,7 +62,12 @@ struct ImageHeader {
     uint64_t off_final;                         // final weights float[S] (0 when the model has no </s>)
     int32_t start_state;                        // state of the context <s> (0 without <s>)
     int32_t has_final;
+    uint64_t off_top_arcs;                      // the order-N arcs
+    int64_t top_arc_begin;                      // first arc of order N (A3 when there is none)
+    int32_t arc_to_delta;                       // next state of arc a of order < N: a + arc_to_delta
+    int32_t pad;
 };
+static_assert(sizeof(ImageHeader) == 248, "the header layout is part of the image format");
 
 struct ChainHead {
     int32_t dense_row;
@@ -76,9 +86,14 @@ static_assert(sizeof(ChainHead) == 16 && sizeof(ChainLevel) == 16, "chain record
 struct Arc {
     int32_t tok;
     float w;
+};
+static_assert(sizeof(Arc) == 8, "an arc below the highest order is two words");
+struct TopArc {
+    int32_t tok;
+    float w;
     int32_t to;
 };
-static_assert(sizeof(Arc) == 12, "an arc is three words");
+static_assert(sizeof(TopArc) == 12, "an arc of the highest order is three words");
 
 // Host-side CSR record (not in the device image): used for byte accounting.
 struct StateRec {
@@ -93,12 +108,15 @@ struct DevTrie {
     const unsigned char *chain;
     const float *dense_w;
     const int32_t *dense_to;
-    const Arc *arcs;
+    const Arc *arcs;          // arcs 0 .. top_begin - 1
+    const TopArc *top_arcs;   // arcs top_begin .. A3 - 1, at a - top_begin
     const float *final_w;   // nullptr without </s>
     int32_t *status;
     int32_t num_states;
     int32_t vocab_size;
     int32_t max_order;
+    int32_t top_begin;      // first arc of the highest order
+    int32_t to_delta;       // next state of an arc below top_begin: its index + to_delta
     int32_t pad;
     int32_t first[NGPU_LM_MAX_ORDER + 1];
     uint64_t off_order[NGPU_LM_MAX_ORDER];

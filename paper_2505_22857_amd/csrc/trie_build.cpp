@@ -360,8 +360,14 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
     off = align_up(off + size_t(R) * size_t(V) * 4);
     h.off_dense_to = off;
     off = align_up(off + size_t(R) * size_t(V) * 4);
+    // arcs of order N: the only ones whose next state is not their own n-gram's
+    const int64_t top_begin = N >= 3 ? arc_base[N] - arc3 : 0;
+    h.top_arc_begin = top_begin;
+    h.arc_to_delta = N > 3 ? int32_t(first[3]) : 0;
     h.off_arcs = off;
-    off = align_up(off + size_t(A3) * sizeof(Arc));
+    off = align_up(off + size_t(top_begin) * sizeof(Arc));
+    h.off_top_arcs = off;
+    off = align_up(off + size_t(A3 - top_begin) * sizeof(TopArc));
     h.has_final = special ? 1 : 0;
     h.off_final = special ? off : 0;
     if (special) off = align_up(off + size_t(S) * 4);
@@ -381,6 +387,9 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
     float *dense_w = reinterpret_cast<float *>(img.data() + h.off_dense_w);
     int32_t *dense_to = reinterpret_cast<int32_t *>(img.data() + h.off_dense_to);
     Arc *arcs = reinterpret_cast<Arc *>(img.data() + h.off_arcs);
+    TopArc *top_arcs = reinterpret_cast<TopArc *>(img.data() + h.off_top_arcs);
+    // token of image arc a (either array)
+    auto arc_tok = [&](int64_t a) { return a < top_begin ? arcs[a].tok : top_arcs[a - top_begin].tok; };
 
     // dense row 0: the empty context (Section 2.2: every token has an arc; missing ones get <unk>)
     for (int32_t v = 0; v < V; ++v) {
@@ -408,14 +417,24 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
             rt[v] = N > 2 ? int32_t(first[2] + a) : int32_t(first[1] + L2.suffix[a]);
         }
     }
-    // sparse arcs of orders 3..N: token, weight, next state
+    // sparse arcs of orders 3..N: token and weight; the next state is the
+    // arc's own n-gram (k < N: first[k] + p = a + first[3], as arc_base[k] -
+    // arc3 and first[k] - first[3] both count the orders 3 .. k-1) or, for
+    // order N, the n-gram's suffix
     for (int k = 3; k <= N; ++k) {
         const OrderLevel &L = lv[k];
         for (size_t p = 0; p < L.key.size(); ++p) {
             int64_t a = arc_base[k] - arc3 + int64_t(p);
-            arcs[a].tok = int32_t(uint64_t(L.key[p]) & tmask);
-            arcs[a].w = L.w[p];
-            arcs[a].to = k < N ? int32_t(first[k] + int64_t(p)) : int32_t(first[N - 1] + L.suffix[p]);
+            const int32_t tok = int32_t(uint64_t(L.key[p]) & tmask);
+            if (k < N) {
+                arcs[a].tok = tok;
+                arcs[a].w = L.w[p];
+            } else {
+                TopArc &ta = top_arcs[a - top_begin];
+                ta.tok = tok;
+                ta.w = L.w[p];
+                ta.to = int32_t(first[N - 1] + L.suffix[p]);
+            }
         }
     }
     // dense-row groups: longest-processing-time assignment of rows, weighted by
@@ -456,7 +475,7 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
         for (int64_t st = first[2 < N ? 2 : N]; N >= 3 && st < S; ++st) {
             uint32_t c[3] = {0, 0, 0};
             for (int32_t a = rec[st].begin; a < rec[st].end; ++a) {
-                const int32_t tok = arcs[a - arc3].tok;
+                const int32_t tok = arc_tok(a - arc3);
                 for (int i = 0; i < 3; ++i) c[i] += tok < 256 * (i + 1) ? 1u : 0u;
             }
             splits[size_t(st)] = c[0] | (c[1] << 9) | (c[2] << 19);

@@ -16,7 +16,9 @@
 //   3. the sparse levels are applied bottom-up (order 2 first, the query
 //      state's order last), each overwriting the slots of its tokens with the
 //      final score and the next state marked kFinal, so the highest order that
-//      holds a token wins, as in Algorithm 1.  Arcs are 12-byte records: up to
+//      holds a token wins, as in Algorithm 1.  Arcs below the highest order
+//      are 8-byte records {token, weight} whose next state is their index plus
+//      a constant; those of the highest order carry it, in 12 bytes.  Up to
 //      four 64-arc stripes of a level are loaded (one load per lane each)
 //      before any of them is written.  When the W wavefronts of a hypothesis
 //      own one 256-token stripe each, every wavefront loads only the arcs of
@@ -32,6 +34,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "trie.h"
 
@@ -57,19 +61,57 @@ __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70
 typedef __attribute__((address_space(1))) const void global_cptr;
 typedef __attribute__((address_space(3))) void lds_ptr;
 
+// Kernel arguments are otherwise loaded (scalar loads) where first used, each
+// waited for before the next is issued; in a latency-bound launch that puts
+// several scalar memory round trips before the first state load.  Passing
+// them to empty asm statements at the kernel's start issues all their loads at
+// once, with one wait; later reads reuse the values (kernel arguments are
+// constant) or hit the scalar cache.  The asm statements count as memory
+// accesses, so uniform loads from global memory after them are vector loads.
+// Used by the small-batch kernels only: kernels with a loop over hypotheses or
+// frames would hold the values in scalar registers throughout and spill.
+template <class T>
+__device__ __forceinline__ void load_arg(const T &v) {
+    asm volatile("" ::"s"(v));
+}
+template <class... T>
+__device__ __forceinline__ void load_args(const T &...v) {
+    (load_arg(v), ...);
+}
+
+__device__ __forceinline__ void load_trie_args(const DevTrie &t) {
+    load_args(t.chain, t.dense_w, t.dense_to, t.arcs, t.top_arcs, t.status, t.num_states, t.vocab_size, t.top_begin,
+              t.to_delta);
+    load_args(t.first[1], t.first[2], t.first[3], t.first[4], t.first[5], t.first[6], t.first[7], t.first[8],
+              t.first[9]);
+    load_args(t.off_order[0], t.off_order[1], t.off_order[2], t.off_order[3], t.off_order[4], t.off_order[5],
+              t.off_order[6], t.off_order[7], t.off_order[8], t.off_order[9]);
+    static_assert(NGPU_LM_MAX_ORDER == 10, "the chain tables above have NGPU_LM_MAX_ORDER entries");
+}
+
 // LDS row length: V rounded up to whole 256-token copy stripes.
 __host__ __device__ inline int lds_row(int V) { return (V + 255) & ~255; }
 
 // Chain record address of state s (s in [0, num_states)) and its number of levels.
+// SGPR_TABLES: every table entry goes through an empty asm, so that the
+// selection stays a chain of selects on values already in scalar registers;
+// otherwise the compiler turns it into one load from a selected address,
+// which waits for the state before it can issue (one more round trip before
+// the record load in a latency-bound launch, but fewer registers held in a
+// kernel that loops over hypotheses or frames).
+template <bool SGPR_TABLES = false>
 __device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, int s, int &nlev) {
     int k = 0, fk = 0;
     uint64_t off = t.off_order[0];
 #pragma unroll
     for (int j = 1; j < NGPU_LM_MAX_ORDER; ++j) {
-        if (s >= t.first[j]) {   // first[] ascends; entries past the last order equal S
+        int32_t f = t.first[j];
+        uint64_t o = t.off_order[j];
+        if (SGPR_TABLES) asm volatile("" : "+s"(f), "+s"(o));
+        if (s >= f) {   // first[] ascends; entries past the last order equal S
             k = j;
-            fk = t.first[j];
-            off = t.off_order[j];
+            fk = f;
+            off = o;
         }
     }
     nlev = k > 1 ? k - 1 : 0;
@@ -172,8 +214,9 @@ constexpr int kBufferConfig = 0x00020000;
 
 // Issues the load of state s's chain record (s uniform and valid); nlev is its
 // number of levels.  The record is consumed by walk_record().
+template <bool SGPR_TABLES = false>
 __device__ __forceinline__ int4 fetch_record(const DevTrie &t, int s, int lane, int &nlev) {
-    const unsigned char *rp = chain_record(t, s, nlev);
+    const unsigned char *rp = chain_record<SGPR_TABLES>(t, s, nlev);
     return load_record(rp, nlev, lane);
 }
 
@@ -228,13 +271,52 @@ __device__ __forceinline__ void dense_stripes_to_lds(const DevTrie &t, int row, 
     }
 }
 
+__device__ __forceinline__ int next_of(const Arc &, int a, int to_delta) { return a + to_delta; }
+__device__ __forceinline__ int next_of(const TopArc &r, int, int) { return r.to; }
+
+// Arcs [a0, end) of one level, all of one order, applied to (ls, ln) with
+// accumulator acc: four 64-arc stripes per round trip.  TOP: the level's arcs
+// are of the highest order, records with their next state (top_arcs); below
+// it an arc's next state is its index plus to_delta.
+template <int W, bool HALVES, bool TOP>
+__device__ __forceinline__ void apply_level(const DevTrie &t, int a0, int end, float acc, float *ls, int *ln,
+                                            int lane, int wave) {
+    typedef typename std::conditional<TOP, TopArc, Arc>::type Rec;
+    const Rec *recs = TOP ? reinterpret_cast<const Rec *>(t.top_arcs) : reinterpret_cast<const Rec *>(t.arcs);
+    const int first = TOP ? t.top_begin : 0;   // index of recs[0]
+    for (; a0 < end; a0 += 4 * kWave) {
+        // (loaded straight into the array, with no copy in the branch that
+        // would have to wait for the load)
+        Rec r[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int a = a0 + u * kWave + lane;
+            if (a < end) r[u] = recs[a - first];
+        }
+        // one wait the compiler sees for all the loads: otherwise, since the
+        // writes below may be skipped, it keeps them pending across the loop
+        // and waits before each load of the next chunk
+        wait_loads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int a = a0 + u * kWave + lane;
+            if (a < end && (HALVES || owns_token<W>(r[u].tok, wave))) {
+                const int slot = HALVES ? r[u].tok - 2 * kStripe * wave : r[u].tok;
+                ls[slot] = acc + r[u].w;
+                ln[slot] = next_of(r[u], a, t.to_delta) | kFinal;
+            }
+        }
+    }
+}
+
 // The walk of a fetched record into (ls, ln), the stripes of wavefront `wave`
 // of W (SPLIT: each wavefront owns exactly one stripe, and loads only its part
-// of each level).  When pf_src is given, pf_n words from it are also copied
-// into pf_dst (the owned stripes) once the record is in (a prefetch that
-// rides along with the dense row and the arcs).  DENSE_ISSUED: the caller
-// already issued the copy of the dense row (before any arc load, which orders
-// the arcs' LDS writes after it).
+// of each level; HALVES: two wavefronts, each owning one 512-token half).
+// When pf_src is given, pf_n words from it are also copied into pf_dst (the
+// owned stripes) once the record is in (a prefetch that rides along with the
+// dense row and the arcs).  DENSE_ISSUED: the caller already issued the copy
+// of the dense row (before any arc load, which orders the arcs' LDS writes
+// after it).
 template <int W = 1, bool SPLIT = false, bool DENSE_ISSUED = false, bool HALVES = false>
 __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &rec, int nlev, float *ls, int *ln,
                                                  int lane, int wave = 0, const float *pf_src = nullptr,
@@ -251,36 +333,20 @@ __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &r
         int a0, end;
         level_bounds<W, SPLIT, HALVES>(rec, j, wave, a0, end);
         const float acc = __int_as_float(__builtin_amdgcn_readlane(rec.z, j));
-        for (; a0 < end; a0 += 4 * kWave) {
-            Arc r[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int a = a0 + u * kWave + lane;
-                if (a < end) r[u] = t.arcs[a];
-            }
-            // one wait the compiler sees for all four loads: otherwise, since
-            // the writes below may be skipped, it keeps them pending across
-            // the loop and waits before each load of the next chunk
-            wait_loads();
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int a = a0 + u * kWave + lane;
-                if (a < end && (HALVES || owns_token<W>(r[u].tok, wave))) {
-                    const int slot = HALVES ? r[u].tok - 2 * kStripe * wave : r[u].tok;
-                    ls[slot] = acc + r[u].w;
-                    ln[slot] = r[u].to | kFinal;
-                }
-            }
-        }
+        if (a0 >= t.top_begin)   // uniform: a level holds arcs of one order
+            apply_level<W, HALVES, true>(t, a0, end, acc, ls, ln, lane, wave);
+        else
+            apply_level<W, HALVES, false>(t, a0, end, acc, ls, ln, lane, wave);
     }
     wait_lds_copies();
     return h;
 }
 
 // The walk of uniform state s into (ls, ln).
+template <bool SGPR_TABLES = false>
 __device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
     int nlev;
-    const int4 rec = fetch_record(t, s, lane, nlev);
+    const int4 rec = fetch_record<SGPR_TABLES>(t, s, lane, nlev);
     return walk_record(t, rec, nlev, ls, ln, lane);
 }
 

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(lib):
     assert sorted(ng.EXPORTED) == decl
 
 
-HDR_FMT = "<IiiiqqQQQQQQ11i4x10QQii"
+HDR_FMT = "<IiiiqqQQQQQQ11i4x10QQiiQqii"
 
 
 def parse_image(img):
@@ -51,13 +51,18 @@ def parse_image(img):
     o_st, o_ch, o_dw, o_dt, o_arc, total = f[6:12]
     first = list(f[12:23])
     off_order = list(f[23:33])
-    off_final, start_state, has_final = f[33:36]
-    assert magic == 0x334D4C4E and total == len(img)
-    arcs = np.frombuffer(raw, np.int32, 3 * A3, o_arc).reshape(A3, 3)   # {token, weight bits, next state}
+    off_final, start_state, has_final, o_top, top_begin, delta = f[33:39]
+    assert struct.calcsize(HDR_FMT) == 248
+    assert magic == 0x344D4C4E and total == len(img)
+    lo = np.frombuffer(raw, np.int32, 2 * top_begin, o_arc).reshape(top_begin, 2)    # {token, weight bits}
+    hi = np.frombuffer(raw, np.int32, 3 * (A3 - top_begin), o_top).reshape(-1, 3)  # {token, weight bits, next}
+    arcs = np.concatenate([lo, hi[:, :2]])
+    # next state: index + delta below the highest order, stored at it
+    to = np.concatenate([np.arange(top_begin, dtype=np.int64) + delta, hi[:, 2]]).astype(np.int32)
     return dict(V=V, N=N, R=R, S=S, A=A3, first=first, off_order=off_order, raw=raw, o_ch=o_ch,
                 dense_w=np.frombuffer(raw, np.float32, R * V, o_dw).reshape(R, V),
                 dense_to=np.frombuffer(raw, np.int32, R * V, o_dt).reshape(R, V),
-                tok=arcs[:, 0].copy(), w=arcs[:, 1].copy().view(np.float32), to=arcs[:, 2].copy(),
+                tok=arcs[:, 0].copy(), w=arcs[:, 1].copy().view(np.float32), to=to,
                 start_state=start_state,
                 final=np.frombuffer(raw, np.float32, S, off_final) if has_final else None)
 

@@ -65,6 +65,7 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
     // hypothesis's stores before the next one's loads are issued.
     wait_loads();
     uint64_t todo = __ballot(mine);
+    const KernargTables ci;
     while (todo) {
         const int i = __builtin_ctzll(todo);
         todo &= todo - 1;
@@ -80,8 +81,8 @@ __global__ __launch_bounds__(HPB * kWave) void advance_kernel(DevTrie t, const i
             }
             continue;
         }
-        const ChainHead h = G == 1 ? walk_into_lds(t, s, ls, ln, lane)
-                                   : walk_into_lds_dense_first(t, s, __builtin_amdgcn_readlane(dense_l, i), ls,
+        const ChainHead h = G == 1 ? walk_into_lds(t, ci, s, ls, ln, lane)
+                                   : walk_into_lds_dense_first(t, ci, s, __builtin_amdgcn_readlane(dense_l, i), ls,
                                                                ln, lane);
         if (VEC) {
             for (int v = lane * 4; v < V; v += 4 * kWave) {
@@ -149,6 +150,7 @@ __global__ __launch_bounds__(kWave) void advance_half_kernel(DevTrie t, const in
     }
     wait_loads();   // as in advance_kernel
     uint64_t todo = __ballot(mine);
+    const KernargTables ci;
     while (todo) {
         const int i = __builtin_ctzll(todo);
         todo &= todo - 1;
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(kWave) void advance_half_kernel(DevTrie t, const in
         }
         dense_half_to_lds(t, __builtin_amdgcn_readlane(dense_l, i), ls, ln, part, lane);
         int nlev;
-        const int4 rec = fetch_record(t, s, lane, nlev);
+        const int4 rec = fetch_record(t, ci, s, lane, nlev);
         const ChainHead h = walk_record<1, false, true, true>(t, rec, nlev, ls, ln, lane, part);
         for (int c = c0; c < V && c < c0 + 2 * kStripe; c += kStripe) {
             const int v = c + 4 * lane;
@@ -218,7 +220,7 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
         return;
     }
     int nlev;
-    const int4 rec = fetch_record<true>(t, s, lane, nlev);
+    const int4 rec = fetch_record(t, SgprTables{}, s, lane, nlev);
     const ChainHead h = walk_record<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave);
     for (int c = kStripe * wave; c < V; c += kStripe * W) {
         if (VEC) {

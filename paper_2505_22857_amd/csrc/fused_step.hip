@@ -237,8 +237,9 @@ __device__ __forceinline__ int first_token_state(const ChainHead &h, const float
 // issued.  Returns the label and updates s; all lanes of all W wavefronts
 // return the same values.
 template <int MODE, int W, bool ROW_PENDING, class Asr, class AfterRecord = NoHook, bool SPLIT = false,
-          bool SGPR_TABLES = false>
-__device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, float rowV, float lambda, int &s,
+          class Index = KernargTables>
+__device__ __forceinline__ int greedy_step(const DevTrie &t, const Index &ci, const Asr &asr, float rowV,
+                                           float lambda, int &s,
                                            int pv, float *ls, int *ln, Exchange *xc, int &xi, int wave, int lane,
                                            const float *pf_src = nullptr, float *pf_dst = nullptr, int pf_n = 0,
                                            AfterRecord after_record = {}) {
@@ -247,7 +248,7 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Asr &asr, flo
     // The chain record is fetched first: in CTC and transducer modes its load
     // overlaps the plain ASR argmax, which may still find that the LM is not needed.
     int nlev;
-    const int4 rec = fetch_record<SGPR_TABLES>(t, s, lane, nlev);
+    const int4 rec = fetch_record(t, ci, s, lane, nlev);
     after_record();
     if (MODE == kCtc || MODE == kTransducer) {
         if (ROW_PENDING) wait_lds_copies();
@@ -336,8 +337,8 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     int xi = 0;
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
-    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, SPLIT, true>(
-        t, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
+    const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, SPLIT>(
+        t, SgprTables{}, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
     if (wave == 0 && lane == 0) {
         tokens[b] = label;
         states[b] = s;
@@ -404,6 +405,7 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
     }
     float rowV = (MODE != kPlain && len > 0) ? row[V] : 0.0f;
     int keep_lab = -1, keep_st = -1, xi = 0;
+    const ChainIndex ci = chain_index(t, lane);
     for (int64_t f = 0; f < len; ++f, row += stride_t) {
         // LDS rows: frame f reads its ASR row from LDS, copied during frame
         // f - 1 (or before the loop); the walk also starts the copy of row
@@ -420,14 +422,14 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
             const float *src = more ? pf : row;
             auto load_next = [&]() { nxt_r.load(src, V, wave, lane); };
             label = greedy_step<MODE, W, false, RegAsr<W, FULL>, decltype(load_next), SPLIT>(
-                t, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr, nullptr, 0, load_next);
+                t, ci, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr, nullptr, 0, load_next);
             cur_r = nxt_r;
         } else {
             float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
             float *nxt = abuf + (kRowBufs == 2 ? ((f + 1) & 1) * rowp : 0);
             label = greedy_step<MODE, W, false, LdsAsr<W>, NoHook, SPLIT>(
-                t, LdsAsr<W>{cur}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, kRowBufs == 2 ? pf : nullptr, nxt,
-                V);
+                t, ci, LdsAsr<W>{cur}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, kRowBufs == 2 ? pf : nullptr,
+                nxt, V);
             // one buffer: every read of this frame's row has completed (its values
             // were consumed by the argmax), so the next row can be copied over it
             if (kRowBufs == 1 && pf) copy_stripes_dword<W>(pf, cur, V, wave, lane);
@@ -502,7 +504,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds<true>(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds(t, SgprTables{}, s, ls, ln, lane);   // its final wait covers the ASR row too
     constexpr int kTaken = int32_t(0x80000000u);
     float bx = -__builtin_inff();
     int bi = kNone;
@@ -597,7 +599,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds<true>(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds(t, SgprTables{}, s, ls, ln, lane);   // its final wait covers the ASR row too
     // value i = 4 c + j of this lane is token 256 c + 4 lane + j
     float f[4 * SPL];
     int n[4 * SPL];
@@ -755,7 +757,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds<true>(t, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds(t, SgprTables{}, s, ls, ln, lane);   // its final wait covers the ASR row too
     // slot i = 4 c + j of this lane is token 256 c + 4 lane + j
     float f[kN];
     int n[kN];

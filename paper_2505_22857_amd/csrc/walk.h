@@ -92,23 +92,77 @@ __device__ __forceinline__ void load_trie_args(const DevTrie &t) {
 // LDS row length: V rounded up to whole 256-token copy stripes.
 __host__ __device__ inline int lds_row(int V) { return (V + 255) & ~255; }
 
-// Chain record address of state s (s in [0, num_states)) and its number of levels.
-// SGPR_TABLES: every table entry goes through an empty asm, so that the
-// selection stays a chain of selects on values already in scalar registers;
-// otherwise the compiler turns it into one load from a selected address,
-// which waits for the state before it can issue (one more round trip before
-// the record load in a latency-bound launch, but fewer registers held in a
-// kernel that loops over hypotheses or frames).
-template <bool SGPR_TABLES = false>
+// Chain record address of state s (s in [0, num_states), one per lane) and its
+// number of levels.
 __device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, int s, int &nlev) {
+    int k = 0, fk = 0;
+    uint64_t off = t.off_order[0];
+#pragma unroll
+    for (int j = 1; j < NGPU_LM_MAX_ORDER; ++j) {
+        if (s >= t.first[j]) {   // first[] ascends; entries past the last order equal S
+            k = j;
+            fk = t.first[j];
+            off = t.off_order[j];
+        }
+    }
+    nlev = k > 1 ? k - 1 : 0;
+    return t.chain + off + size_t(s - fk) * 16u * size_t(k > 0 ? k : 1);
+}
+
+// The per-order tables of chain_record spread over the lanes of a wavefront,
+// built once per kernel: lane j (1 <= j < NGPU_LM_MAX_ORDER) holds first[j],
+// every other lane a bound no state reaches, and lane j holds base[j] with
+// record(s) = chain + base[k] + 16 max(k, 1) s for a state s of order k.  A
+// uniform state's order is then one compare, a ballot and a popcount, and its
+// base one pair of readlanes: no memory access and no scalar registers held
+// across the loops of the kernels (the tables from the kernel arguments would
+// be loaded again at every use there).
+struct ChainIndex {
+    int32_t first;
+    uint64_t base;
+};
+
+__device__ __forceinline__ ChainIndex chain_index(const DevTrie &t, int lane) {
+    ChainIndex ci{0x7fffffff, 0};
+#pragma unroll
+    for (int j = 0; j < NGPU_LM_MAX_ORDER; ++j) {
+        if (lane == j) {
+            const int32_t f = j == 0 ? 0 : t.first[j];
+            ci.first = j == 0 ? 0x7fffffff : f;
+            ci.base = t.off_order[j] - uint64_t(16 * (j > 0 ? j : 1)) * uint64_t(f);
+        }
+    }
+    return ci;
+}
+
+// How a kernel finds the record of a uniform state (every lane of the
+// wavefront active), by the lifetime of the kernel:
+//  - KernargTables: the tables from the kernel arguments where used (the
+//    compiler turns the selection into one load from a selected address,
+//    after the state has arrived); the plain choice for kernels that walk many
+//    hypotheses each;
+//  - SgprTables: every table entry through an empty asm, so the selection
+//    stays a chain of selects on values already in scalar registers: no load
+//    between the state and its record, for one-shot latency-bound kernels;
+//  - ChainIndex (above): for kernels that loop over frames, where the tables
+//    in scalar registers would spill and from the kernel arguments would be
+//    loaded again at every use.
+struct KernargTables {};
+struct SgprTables {};
+
+__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, KernargTables, int s, int &nlev) {
+    return chain_record(t, s, nlev);
+}
+
+__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, SgprTables, int s, int &nlev) {
     int k = 0, fk = 0;
     uint64_t off = t.off_order[0];
 #pragma unroll
     for (int j = 1; j < NGPU_LM_MAX_ORDER; ++j) {
         int32_t f = t.first[j];
         uint64_t o = t.off_order[j];
-        if (SGPR_TABLES) asm volatile("" : "+s"(f), "+s"(o));
-        if (s >= f) {   // first[] ascends; entries past the last order equal S
+        asm volatile("" : "+s"(f), "+s"(o));
+        if (s >= f) {
             k = j;
             fk = f;
             off = o;
@@ -116,6 +170,15 @@ __device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, i
     }
     nlev = k > 1 ? k - 1 : 0;
     return t.chain + off + size_t(s - fk) * 16u * size_t(k > 0 ? k : 1);
+}
+
+__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, const ChainIndex &ci, int s,
+                                                            int &nlev) {
+    const int k = __builtin_popcountll(__ballot(s >= ci.first));
+    const uint64_t base = (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(ci.base >> 32), k))) << 32) |
+                          uint32_t(__builtin_amdgcn_readlane(int(uint32_t(ci.base)), k));
+    nlev = k > 1 ? k - 1 : 0;
+    return t.chain + base + uint64_t(s) * uint64_t(16 * (k > 0 ? k : 1));
 }
 
 __device__ __forceinline__ int chain_group(const ChainHead &h) { return h.nlev_group >> 16; }
@@ -214,9 +277,9 @@ constexpr int kBufferConfig = 0x00020000;
 
 // Issues the load of state s's chain record (s uniform and valid); nlev is its
 // number of levels.  The record is consumed by walk_record().
-template <bool SGPR_TABLES = false>
-__device__ __forceinline__ int4 fetch_record(const DevTrie &t, int s, int lane, int &nlev) {
-    const unsigned char *rp = chain_record<SGPR_TABLES>(t, s, nlev);
+template <class Index>
+__device__ __forceinline__ int4 fetch_record(const DevTrie &t, const Index &ci, int s, int lane, int &nlev) {
+    const unsigned char *rp = chain_record(t, ci, s, nlev);
     return load_record(rp, nlev, lane);
 }
 
@@ -343,21 +406,23 @@ __device__ __forceinline__ ChainHead walk_record(const DevTrie &t, const int4 &r
 }
 
 // The walk of uniform state s into (ls, ln).
-template <bool SGPR_TABLES = false>
-__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, int s, float *ls, int *ln, int lane) {
+template <class Index>
+__device__ __forceinline__ ChainHead walk_into_lds(const DevTrie &t, const Index &ci, int s, float *ls, int *ln,
+                                                   int lane) {
     int nlev;
-    const int4 rec = fetch_record<SGPR_TABLES>(t, s, lane, nlev);
+    const int4 rec = fetch_record(t, ci, s, lane, nlev);
     return walk_record(t, rec, nlev, ls, ln, lane);
 }
 
 // The same walk when the state's dense row is already known (from its chain
 // head): the row's copy into LDS goes out before the record load, so the two
 // overlap instead of the copy waiting for the record.
-__device__ __forceinline__ ChainHead walk_into_lds_dense_first(const DevTrie &t, int s, int dense_row, float *ls,
-                                                               int *ln, int lane) {
+template <class Index>
+__device__ __forceinline__ ChainHead walk_into_lds_dense_first(const DevTrie &t, const Index &ci, int s,
+                                                               int dense_row, float *ls, int *ln, int lane) {
     dense_to_lds(t, dense_row, ls, ln, lane);
     int nlev;
-    const int4 rec = fetch_record(t, s, lane, nlev);
+    const int4 rec = fetch_record(t, ci, s, lane, nlev);
     return walk_record<1, false, true>(t, rec, nlev, ls, ln, lane);
 }
 

@@ -211,6 +211,7 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
     float *orow = scores + b * V;
     int32_t *nrow = next + b * V;
     const int s = __builtin_amdgcn_readfirstlane(states[b]);
+    const ChainIndex ci = chain_index(t, lane);
     if (s < 0 || s >= t.num_states) {
         if (wave == 0 && lane == 0) atomicAdd(&t.status[0], 1);
         for (int v = wave * kWave + lane; v < V; v += W * kWave) {
@@ -220,7 +221,7 @@ __global__ __launch_bounds__(W * kWave) void advance_striped_kernel(DevTrie t, c
         return;
     }
     int nlev;
-    const int4 rec = fetch_record(t, SgprTables{}, s, lane, nlev);
+    const int4 rec = fetch_record(t, ci, s, lane, nlev);
     const ChainHead h = walk_record<W, SPLIT>(t, rec, nlev, ls, ln, lane, wave);
     for (int c = kStripe * wave; c < V; c += kStripe * W) {
         if (VEC) {

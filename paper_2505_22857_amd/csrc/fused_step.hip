@@ -323,6 +323,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     const int pv_l = MODE == kCtc ? prev[b] : -1;
     const float rowV_l = MODE == kPlain ? 0.0f : src[V];
     copy_stripes_dword<W>(src, arow, V, wave, lane);
+    const ChainIndex ci = chain_index(t, lane);
     int s = __builtin_amdgcn_readfirstlane(s_l);
     const int pv = __builtin_amdgcn_readfirstlane(pv_l);
     const float rowV = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, rowV_l)));
@@ -338,7 +339,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
     // every wavefront has read states[b] and prev[b] before the first exchange
     // barrier inside the step, and wavefront 0 writes them back after it
     const int label = greedy_step<MODE, W, true, LdsAsr<W>, NoHook, SPLIT>(
-        t, SgprTables{}, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
+        t, ci, LdsAsr<W>{arow}, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane);
     if (wave == 0 && lane == 0) {
         tokens[b] = label;
         states[b] = s;
@@ -493,6 +494,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     int32_t *onx = next + b * k;
     const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
     copy_to_lds_dword(asr + b * ld, arow, V, lane);
+    const ChainIndex ci = chain_index(t, lane);
     const int s = __builtin_amdgcn_readfirstlane(s_l);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, SgprTables{}, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds(t, ci, s, ls, ln, lane);   // its final wait covers the ASR row too
     constexpr int kTaken = int32_t(0x80000000u);
     float bx = -__builtin_inff();
     int bi = kNone;
@@ -588,6 +590,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
     int32_t *onx = next + b * k;
     const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
     copy_to_lds_dword(asr + b * ld, arow, V, lane);
+    const ChainIndex ci = chain_index(t, lane);
     const int s = __builtin_amdgcn_readfirstlane(s_l);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
@@ -599,7 +602,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const 
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, SgprTables{}, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds(t, ci, s, ls, ln, lane);   // its final wait covers the ASR row too
     // value i = 4 c + j of this lane is token 256 c + 4 lane + j
     float f[4 * SPL];
     int n[4 * SPL];
@@ -746,6 +749,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
     int32_t *onx = next + b * k;
     const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
     copy_to_lds_dword(asr + b * ld, arow, V, lane);
+    const ChainIndex ci = chain_index(t, lane);
     const int s = __builtin_amdgcn_readfirstlane(s_l);
     if (s < 0 || s >= t.num_states) {
         if (lane == 0) atomicAdd(&t.status[0], 1);
@@ -757,7 +761,7 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
         wait_lds_copies();   // no copy into LDS outlives the wavefront
         return;
     }
-    const ChainHead h = walk_into_lds(t, SgprTables{}, s, ls, ln, lane);   // its final wait covers the ASR row too
+    const ChainHead h = walk_into_lds(t, ci, s, ls, ln, lane);   // its final wait covers the ASR row too
     // slot i = 4 c + j of this lane is token 256 c + 4 lane + j
     float f[kN];
     int n[kN];

@@ -122,6 +122,8 @@ struct ChainIndex {
     uint64_t base;
 };
 
+// (The empty asm keeps the compiler from moving the construction down to the
+// first lookup, after the state load it is meant to overlap.)
 __device__ __forceinline__ ChainIndex chain_index(const DevTrie &t, int lane) {
     ChainIndex ci{0x7fffffff, 0};
 #pragma unroll
@@ -132,44 +134,25 @@ __device__ __forceinline__ ChainIndex chain_index(const DevTrie &t, int lane) {
             ci.base = t.off_order[j] - uint64_t(16 * (j > 0 ? j : 1)) * uint64_t(f);
         }
     }
+    asm volatile("" ::"v"(ci.first), "v"(ci.base));
     return ci;
 }
 
 // How a kernel finds the record of a uniform state (every lane of the
-// wavefront active), by the lifetime of the kernel:
+// wavefront active):
 //  - KernargTables: the tables from the kernel arguments where used (the
 //    compiler turns the selection into one load from a selected address,
-//    after the state has arrived); the plain choice for kernels that walk many
-//    hypotheses each;
-//  - SgprTables: every table entry through an empty asm, so the selection
-//    stays a chain of selects on values already in scalar registers: no load
-//    between the state and its record, for one-shot latency-bound kernels;
-//  - ChainIndex (above): for kernels that loop over frames, where the tables
-//    in scalar registers would spill and from the kernel arguments would be
-//    loaded again at every use.
+//    after the state has arrived); the choice of the grouped advance, which
+//    walks many hypotheses per wavefront;
+//  - ChainIndex (above), built where the kernel starts: its order from one
+//    compare, a ballot and a popcount, its base from two readlanes.  Holding
+//    the tables in scalar registers instead costs about a hundred scalar
+//    instructions per lookup (a select per order for the order, the offset
+//    and the first id), and makes the decode spill.
 struct KernargTables {};
-struct SgprTables {};
 
 __device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, KernargTables, int s, int &nlev) {
     return chain_record(t, s, nlev);
-}
-
-__device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, SgprTables, int s, int &nlev) {
-    int k = 0, fk = 0;
-    uint64_t off = t.off_order[0];
-#pragma unroll
-    for (int j = 1; j < NGPU_LM_MAX_ORDER; ++j) {
-        int32_t f = t.first[j];
-        uint64_t o = t.off_order[j];
-        asm volatile("" : "+s"(f), "+s"(o));
-        if (s >= f) {
-            k = j;
-            fk = f;
-            off = o;
-        }
-    }
-    nlev = k > 1 ? k - 1 : 0;
-    return t.chain + off + size_t(s - fk) * 16u * size_t(k > 0 ? k : 1);
 }
 
 __device__ __forceinline__ const unsigned char *chain_record(const DevTrie &t, const ChainIndex &ci, int s,

@@ -248,10 +248,13 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Index &ci, co
     // The chain record is fetched first: in CTC and transducer modes its load
     // overlaps the plain ASR argmax, which may still find that the LM is not needed.
     int nlev;
+    if (ROW_PENDING) memory_order_point();   // the ASR row's copies were issued before the record load
     const int4 rec = fetch_record(t, ci, s, lane, nlev);
     after_record();
     if (MODE == kCtc || MODE == kTransducer) {
-        if (ROW_PENDING) wait_lds_copies();
+        // the row, not the record: the record load (one instruction; after_record
+        // adds none when the row is pending) stays in flight through the argmax
+        if (ROW_PENDING) wait_lds_copies_but_last();
         float bx = -__builtin_inff(), av;
         int bi = kNone, unused;
         asr.argmax(V, wave, lane, bx, bi);

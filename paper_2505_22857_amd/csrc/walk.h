@@ -53,6 +53,13 @@ static_assert(int64_t(kStateMask) + 1 == NGPU_LM_MAX_STATES, "state ids fit the 
 // access across the wait.
 __device__ __forceinline__ void wait_lds_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// The same wait when exactly one vector memory instruction was issued after
+// the last copy (vector memory loads complete in order): that one may stay in
+// flight.  Callers put a compiler barrier (memory_order_point) between the
+// copies and that instruction, so the compiler cannot move it above them.
+__device__ __forceinline__ void wait_lds_copies_but_last() { asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); }
+__device__ __forceinline__ void memory_order_point() { asm volatile("" ::: "memory"); }
+
 // vmcnt(0) as an instruction the compiler's wait insertion accounts for
 // (expcnt and lgkmcnt at their maximum: no wait on them); for waits on
 // loads into registers, whose data dependences already order their users.

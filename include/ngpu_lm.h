@@ -222,10 +222,10 @@ int ngpu_lm_fused_greedy_step(const ngpu_lm *lm, const float *d_asr, int64_t B, 
  * than k tokens score above -inf, the rest follow in index order (as a strict
  * '>' selection gives).  States are read only.
  * 1 <= k <= min(V, NGPU_LM_MAX_TOPK); cost per hypothesis: one pass over the V
- * tokens, then for k < 6 (or V > 1024) per selected token one wavefront
- * reduction and a rescan of the V / 64 tokens of one lane, otherwise a
- * selection whose cost hardly grows with k (a binary search for the k-th
- * value, then ranking the k taken tokens).  An out-of-range state gives a
+ * tokens, then for V <= 1024 a selection whose cost hardly grows with k (a
+ * binary search for the k-th value, then ranking the k taken tokens), for
+ * larger V per selected token one wavefront reduction and a rescan of the
+ * V / 64 tokens of one lane.  An out-of-range state gives a
  * row of -1 tokens, NaN scores and -1 states and is counted for
  * ngpu_lm_check_states.  Asynchronous. */
 int ngpu_lm_fused_topk(const ngpu_lm *lm, const float *d_asr, int64_t B, int64_t asr_ld, float lambda, int32_t k,

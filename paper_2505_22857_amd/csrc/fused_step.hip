@@ -563,105 +563,6 @@ __global__ __launch_bounds__(kWave) void fused_topk_kernel(DevTrie t, const floa
     }
 }
 
-// The same selection for V <= 256 * SPL with each lane's 4 * SPL fused values
-// and next states held in registers.  A taken token's value becomes -inf (so
-// the owner's rescan is one compare per token) and its bit is set in the
-// lane's mask (the tokens past V start set); the mask only serves the
-// fallback once every remaining value is -inf.  Register arrays are indexed
-// with compile-time indices only (unrolled loops with a uniform compare), so
-// they stay in registers.
-template <int SPL>
-__global__ __launch_bounds__(kWave) void fused_topk_reg_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
-                                                               int64_t ld, float lambda, int k,
-                                                               const int32_t *__restrict__ states,
-                                                               int32_t *__restrict__ tokens,
-                                                               float *__restrict__ scores,
-                                                               int32_t *__restrict__ next) {
-    static_assert(4 * SPL <= 32, "the taken mask holds 32 tokens per lane");
-    extern __shared__ float lds[];
-    load_trie_args(t);
-    load_args(asr, B, ld, lambda, k, states, tokens, scores, next);
-    const int lane = threadIdx.x;
-    const int64_t b = blockIdx.x;
-    if (b >= B) return;
-    const int V = t.vocab_size;
-    float *ls = lds;
-    int *ln = reinterpret_cast<int *>(ls + lds_row(V));
-    float *arow = reinterpret_cast<float *>(ln + lds_row(V));
-    int32_t *otok = tokens + b * k;
-    float *osc = scores + b * k;
-    int32_t *onx = next + b * k;
-    const int s_l = states[b];   // issued before the row copy, so its wait leaves the copy in flight
-    copy_to_lds_dword(asr + b * ld, arow, V, lane);
-    const ChainIndex ci = chain_index(t, lane);
-    const int s = __builtin_amdgcn_readfirstlane(s_l);
-    if (s < 0 || s >= t.num_states) {
-        if (lane == 0) atomicAdd(&t.status[0], 1);
-        for (int j = lane; j < k; j += kWave) {
-            otok[j] = -1;
-            osc[j] = NAN;
-            onx[j] = -1;
-        }
-        wait_lds_copies();   // no copy into LDS outlives the wavefront
-        return;
-    }
-    const ChainHead h = walk_into_lds(t, ci, s, ls, ln, lane);   // its final wait covers the ASR row too
-    // value i = 4 c + j of this lane is token 256 c + 4 lane + j
-    float f[4 * SPL];
-    int n[4 * SPL];
-    unsigned taken = 0;
-    float bx = -__builtin_inff();
-    int bi = kNone;
-#pragma unroll
-    for (int c = 0; c < SPL; ++c) {
-        const int v0 = c * kStripe + 4 * lane;
-        const f32x4 x = *reinterpret_cast<const f32x4 *>(ls + v0);
-        const i32x4 m = *reinterpret_cast<const i32x4 *>(ln + v0);
-        const f32x4 a = *reinterpret_cast<const f32x4 *>(arow + v0);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            float lm;
-            int nx;
-            slot_value(h, x[j], m[j], lm, nx);
-            const bool in = v0 + j < V;
-            f[4 * c + j] = in ? __builtin_fmaf(lambda, lm, a[j]) : -__builtin_inff();
-            n[4 * c + j] = nx;
-            if (!in) taken |= 1u << (4 * c + j);
-            take_max(f[4 * c + j], v0 + j, bx, bi);
-        }
-    }
-    for (int r = 0; r < k; ++r) {
-        float wv;
-        int w = wave_argmax(bx, bi, wv);
-        if (w == kNone) {   // everything left is -inf: the lowest index not yet taken
-            const unsigned left = ~taken & (SPL == 8 ? 0xffffffffu : (1u << (4 * SPL)) - 1u);
-            const int i = left ? __builtin_ctz(left) : -1;
-            const int lo = i < 0 ? kNone : (i >> 2) * kStripe + 4 * lane + (i & 3);
-            w = int(~wave_max_u32(~(unsigned)lo));
-        }
-        const int wi = (w >> 8) * 4 + (w & 3);   // uniform: the winner's value index in its owner
-        if (lane == ((w & (kStripe - 1)) >> 2)) {   // the lane that owns token w
-            float fv = 0.0f;
-            int nv = 0;
-#pragma unroll
-            for (int i = 0; i < 4 * SPL; ++i)
-                if (i == wi) {
-                    fv = f[i];
-                    nv = n[i];
-                    f[i] = -__builtin_inff();
-                }
-            otok[r] = w;
-            osc[r] = fv;
-            onx[r] = nv;
-            taken |= 1u << wi;
-            bx = -__builtin_inff();
-            bi = kNone;
-#pragma unroll
-            for (int i = 0; i < 4 * SPL; ++i) take_max(f[i], (i >> 2) * kStripe + 4 * lane + (i & 3), bx, bi);
-        }
-    }
-}
-
 // Inclusive prefix sum over the lanes of a wave (the DPP pattern of
 // wave_max_u32 with additions).
 template <int CTRL, int ROW_MASK>
@@ -825,12 +726,9 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
     }
     // 2. taken entries: every key >= T when exact; otherwise T is the k-th
     // key itself, `above` keys exceed it, and of the keys equal to it the
-    // lowest token indices are taken
-    bool take[kN];
-    if (exact) {
-#pragma unroll
-        for (int i = 0; i < kN; ++i) take[i] = key[i] >= T;
-    } else {
+    // lowest token indices are taken (bit i of tie_taken: slot i is such a tie)
+    unsigned tie_taken = 0;
+    if (!exact) {
         const int ties_needed = k - above;
         int ties_before = 0;   // ties at T in earlier stripes (uniform)
 #pragma unroll
@@ -848,30 +746,39 @@ __global__ __launch_bounds__(kWave) void fused_topk_select_kernel(DevTrie t, con
             for (int j = 0; j < 4; ++j) {
                 const int i = 4 * c + j;
                 const bool tie = key[i] == T;
-                take[i] = key[i] > T || (tie && ties_before + below + own < ties_needed);
+                if (tie && ties_before + below + own < ties_needed) tie_taken |= 1u << i;
                 own += tie ? 1 : 0;
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) ties_before += __builtin_popcountll(m[j]);
         }
     }
-    // 3. compaction into LDS (the walked row is in registers now), then ranks
+    // 3. compaction into LDS (the walked row is in registers now), then ranks;
+    // the exact case tests its keys directly, with no per-slot flags to build
     unsigned long long *sk = reinterpret_cast<unsigned long long *>(lds);
     float *ssc = reinterpret_cast<float *>(sk + k);
     int *snx = reinterpret_cast<int *>(ssc + k);
-    int base = 0;
+    auto compact = [&](auto taken) {
+        int base = 0;
 #pragma unroll
-    for (int i = 0; i < kN; ++i) {
-        const unsigned long long m = __ballot(take[i]);
-        if (take[i]) {
-            const int p = base + int(__builtin_amdgcn_mbcnt_hi(unsigned(m >> 32), __builtin_amdgcn_mbcnt_lo(unsigned(m), 0u)));
-            const int tok = (i >> 2) * kStripe + 4 * lane + (i & 3);
-            sk[p] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~unsigned(tok));
-            ssc[p] = f[i];
-            snx[p] = n[i];
+        for (int i = 0; i < kN; ++i) {
+            const bool tk = taken(i);
+            const unsigned long long m = __ballot(tk);
+            if (tk) {
+                const int p = base + int(__builtin_amdgcn_mbcnt_hi(unsigned(m >> 32),
+                                                                  __builtin_amdgcn_mbcnt_lo(unsigned(m), 0u)));
+                const int tok = (i >> 2) * kStripe + 4 * lane + (i & 3);
+                sk[p] = (static_cast<unsigned long long>(key[i]) << 32) | unsigned(~unsigned(tok));
+                ssc[p] = f[i];
+                snx[p] = n[i];
+            }
+            base += __builtin_popcountll(m);
         }
-        base += __builtin_popcountll(m);
-    }
+    };
+    if (exact)
+        compact([&](int i) { return key[i] >= T; });
+    else
+        compact([&](int i) { return key[i] > T || ((tie_taken >> i) & 1u) != 0; });
     if (k <= kWave)
         rank_and_store<1>(sk, ssc, snx, k, lane, otok, osc, onx);
     else if (k <= 2 * kWave)
@@ -899,56 +806,34 @@ hipError_t launch_final_weights(const DevTrie &t, const int32_t *states, int64_t
     return hipGetLastError();
 }
 
-// From this k on, the threshold selection beats one reduction per selected
-// token (register layouts, V <= 1024; 1024 hypotheses of the 20M 6-gram:
-// 10.3 against 10.7 us at k = 6, 10.6 against 11.4 at k = 8; 10.9 against
-// 10.7 at k = 4).
-constexpr int kTopkSelectMinK = 6;
-
 hipError_t launch_fused_topk(const DevTrie &t, const float *asr, int64_t B, int64_t ld, float lambda, int k,
                              const int32_t *states, int32_t *tokens, float *scores, int32_t *next,
                              hipStream_t stream) {
     const size_t lds = (2 * size_t(lds_row(t.vocab_size)) + size_t(asr_row_words(t.vocab_size))) * sizeof(float);
     const dim3 grid(static_cast<unsigned>(B)), block(kWave);
     const int spl = (t.vocab_size + kStripe - 1) / kStripe;   // stripes per lane
-    if (k >= kTopkSelectMinK && spl <= 4) {
-        // the k taken entries (16 bytes each) may need more LDS than the row
-        const size_t lds_sel = lds > 16 * size_t(k) ? lds : 16 * size_t(k);
-        switch (spl) {
-            case 1:
-                hipLaunchKernelGGL(fused_topk_select_kernel<1>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
-                                   states, tokens, scores, next);
-                break;
-            case 2:
-                hipLaunchKernelGGL(fused_topk_select_kernel<2>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
-                                   states, tokens, scores, next);
-                break;
-            case 3:
-                hipLaunchKernelGGL(fused_topk_select_kernel<3>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
-                                   states, tokens, scores, next);
-                break;
-            default:
-                hipLaunchKernelGGL(fused_topk_select_kernel<4>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
-                                   states, tokens, scores, next);
-        }
-        return hipGetLastError();
-    }
+    // V <= 1024: the selection with the row in registers, for every k (from
+    // k = 6 on it beats one reduction per selected token; below that the two
+    // are level: 10.1-10.5 us either way at k = 1 to 5 for 1024 hypotheses of
+    // the 20M 6-gram).  Larger V: one reduction per selected token.  The k
+    // taken entries (16 bytes each) may need more LDS than the row.
+    const size_t lds_sel = lds > 16 * size_t(k) ? lds : 16 * size_t(k);
     switch (spl) {
         case 1:
-            hipLaunchKernelGGL(fused_topk_reg_kernel<1>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
-                               tokens, scores, next);
+            hipLaunchKernelGGL(fused_topk_select_kernel<1>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
+                               states, tokens, scores, next);
             break;
         case 2:
-            hipLaunchKernelGGL(fused_topk_reg_kernel<2>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
-                               tokens, scores, next);
+            hipLaunchKernelGGL(fused_topk_select_kernel<2>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
+                               states, tokens, scores, next);
             break;
         case 3:
-            hipLaunchKernelGGL(fused_topk_reg_kernel<3>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
-                               tokens, scores, next);
+            hipLaunchKernelGGL(fused_topk_select_kernel<3>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
+                               states, tokens, scores, next);
             break;
         case 4:
-            hipLaunchKernelGGL(fused_topk_reg_kernel<4>, grid, block, lds, stream, t, asr, B, ld, lambda, k, states,
-                               tokens, scores, next);
+            hipLaunchKernelGGL(fused_topk_select_kernel<4>, grid, block, lds_sel, stream, t, asr, B, ld, lambda, k,
+                               states, tokens, scores, next);
             break;
         default:
             hipLaunchKernelGGL(fused_topk_kernel, grid, block, lds, stream, t, asr, B, ld, lambda, k, states, tokens,

@@ -24,6 +24,8 @@
 // final weight (the </s> score, precomputed per state); <eos> keeps the state.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "walk.h"
 
 namespace ngpu {
@@ -914,16 +916,31 @@ static hipError_t launch_decode_w(const DevTrie &t, const float *asr, int64_t B,
 }
 
 // Utterances the device holds at once with two ASR row buffers per utterance
-// (one wavefront each): CUs times the workgroups whose LDS fits one CU.
+// (one wavefront each): CUs times the workgroups whose LDS fits one CU.  The
+// two device attributes are queried once per device and kept (a decode call
+// then costs one hipGetDevice on the host for this).
 static int64_t resident_double_buffered(const DevTrie &t) {
-    int dev = 0, cus = 0, lds = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess) {
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int64_t> cached[kMaxDevices];   // CUs << 32 | LDS bytes per CU; 0: not yet known
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
         (void)hipGetLastError();
         return INT64_MAX;   // unknown: keep two buffers
     }
-    return int64_t(cus) * int64_t(size_t(lds) / hyp_lds_bytes(t.vocab_size, 2));
+    int64_t c = dev < kMaxDevices ? cached[dev].load(std::memory_order_relaxed) : 0;
+    if (c == 0) {
+        int cus = 0, lds = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess ||
+            cus <= 0 || lds <= 0) {
+            (void)hipGetLastError();
+            return INT64_MAX;
+        }
+        c = (int64_t(cus) << 32) | int64_t(uint32_t(lds));
+        if (dev < kMaxDevices) cached[dev].store(c, std::memory_order_relaxed);
+    }
+    const int64_t cus = c >> 32, lds = c & 0xffffffff;
+    return cus * int64_t(size_t(lds) / hyp_lds_bytes(t.vocab_size, 2));
 }
 
 template <int MODE>

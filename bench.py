@@ -12,8 +12,10 @@ second over the timed steps.  The same run also reports:
   mean kernel duration from HIP events on the launch stream, against 8 TB/s;
   ``traffic`` is the measured HBM bytes per launch from the committed rocprofv3
   counter summary when it was taken on the current kernel source, else null;
-* latency of a single 512-hypothesis call (median of 100), with its
-  algorithmic bytes as a fraction of the HBM roofline (roofline_b512_single);
+* latency of a single 512-hypothesis call (median of 100, the calls enqueued
+  ahead of the GPU so that the events bracket device time; also the same
+  with the GPU waiting for each call's submission), with its algorithmic
+  bytes as a fraction of the HBM roofline (roofline_b512_single);
 * the same work as 128 separate 512-hypothesis calls on 8 streams, captured in
   one HIP graph, likewise against the roofline (roofline_b512_graph);
 * the transducer mode, one launch per step, at 32 and 256 hypotheses;
@@ -152,24 +154,37 @@ def main():
     for _ in range(10):
         lm.advance(states[:Bb], s512, n512)
     torch.cuda.synchronize()
-    lat = []
-    for r in range(100):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        sl = slice((r % R) * Bb, (r % R + 1) * Bb)
-        st_r, sc_r, nx_r = states[sl], scores[sl], nxt[sl]   # views made outside the timed bracket
-        e0.record(stream)
-        lm.advance(st_r, sc_r, nx_r)
-        e1.record(stream)
-        lat.append((e0, e1))
-    torch.cuda.synchronize()
-    lat_us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in lat]))
-    log(f"single B={Bb} call: median {lat_us:.1f} us")
+
+    def single_calls(queued):
+        # queued: the GPU first spins for a few ms, so the host enqueues all
+        # calls ahead and each event pair brackets the call's device time only;
+        # otherwise the GPU waits for each call's host-side submission, which
+        # the bracket then includes
+        views = [(states[sl], scores[sl], nxt[sl]) for sl in
+                 (slice((r % R) * Bb, (r % R + 1) * Bb) for r in range(100))]
+        lat = []
+        if queued:
+            torch.cuda._sleep(int(8e6))
+        for st_r, sc_r, nx_r in views:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            lm.advance(st_r, sc_r, nx_r)
+            e1.record(stream)
+            lat.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) * 1e3 for a, b in lat]))
+
+    lat_host_us = single_calls(False)
+    lat_us = single_calls(True)
+    log(f"single B={Bb} call: median {lat_us:.1f} us of device time ({lat_host_us:.1f} us paced by the host)")
     # algorithmic bytes of one 512-hypothesis call: the mean over the slices the 100 calls cycle through
     call_bytes = float(np.mean([lm.query_bytes(states_np[(r % R) * Bb:(r % R + 1) * Bb])[0] for r in range(100)]))
     single = {"bound": "hbm", "achieved": call_bytes / (lat_us * 1e-6) / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
               "frac": call_bytes / (lat_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, "bytes_per_call": call_bytes,
-              "us_per_call": lat_us,
-              "workload": f"one advance call of B={Bb} uniform states (median of 100, HIP events around the call)"}
+              "us_per_call": lat_us, "us_per_call_host_paced": lat_host_us,
+              "workload": f"one advance call of B={Bb} uniform states (median of 100, HIP events around each "
+                          f"call, enqueued ahead of the GPU; us_per_call_host_paced: the GPU idle until each "
+                          f"call is submitted)"}
 
     # ---- sustained: one launch over all R batches per step
     for _ in range(args.warmup):

@@ -302,7 +302,6 @@ static hipError_t launch_hpb(const DevTrie &t, const int32_t *states, int64_t B,
 //    9.4 us at 128 hypotheses, 9.0 against 9.9 at 512, 9.6 against 10.0 at
 //    1024; 10.7 against 10.5 at 1536 and 12.1 against 11.2 at 2048.
 constexpr int64_t kStripedMaxBatch = 1024;
-constexpr bool kAdvanceHalves = true;
 constexpr int64_t kGroupedMinBatch = 20480;
 constexpr int kHpbGrouped = 1;
 constexpr int kHpbPlain = 2;
@@ -321,7 +320,7 @@ hipError_t launch_advance(const DevTrie &t, const int32_t *states, int64_t B, fl
                      (reinterpret_cast<uintptr_t>(next) % 16 == 0);
     if (B >= kGroupedMinBatch) {
         const int64_t chunks = (B + kGroups - 1) / kGroups;
-        if (vec && kAdvanceHalves && (t.vocab_size + kStripe - 1) / kStripe == 4 &&
+        if (vec && (t.vocab_size + kStripe - 1) / kStripe == 4 &&
             2 * chunks * kGroups * kWave <= int64_t(UINT32_MAX)) {   // dispatch size in work-items
             hipLaunchKernelGGL(advance_half_kernel<kGroups>, dim3(unsigned(2 * chunks * kGroups)), dim3(kWave),
                                size_t(4 * kStripe) * sizeof(float), stream, t, states, B, scores, next);

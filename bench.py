@@ -17,7 +17,9 @@ second over the timed steps.  The same run also reports:
   with the GPU waiting for each call's submission), with its algorithmic
   bytes as a fraction of the HBM roofline (roofline_b512_single);
 * the same work as 128 separate 512-hypothesis calls on 8 streams, captured in
-  one HIP graph, likewise against the roofline (roofline_b512_graph);
+  one HIP graph, likewise against the roofline (roofline_b512_graph), with
+  the host time of each replay call and the GPU's own time per replay when
+  the replays are enqueued ahead of it;
 * the transducer mode, one launch per step, at 32 and 256 hypotheses;
 * the fused greedy CTC step at B = 256 utterances, 1025 classes, per frame,
   and the same decode of 1000 frames as one launch;
@@ -235,19 +237,43 @@ def main():
         torch.cuda.synchronize()
         reps = 20
         g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t_host = time.perf_counter()
         g0.record(stream)
         for _ in range(reps):
             g_adv.replay()
         g1.record(stream)
+        host_ms = (time.perf_counter() - t_host) * 1e3 / reps
         torch.cuda.synchronize()
-        assert lm.check_states() == 0
         g_ms = g0.elapsed_time(g1) / reps
+        # the same replays enqueued while the GPU spins, so they run back to
+        # back at the GPU's own pace: valid only if the host finished
+        # enqueueing before the spin ended
+        gs = torch.cuda.Event(enable_timing=True)
+        gs.record(stream)
+        torch.cuda._sleep(int(4e7))
+        g0.record(stream)
+        t_host = time.perf_counter()
+        for _ in range(reps):
+            g_adv.replay()
+        enqueue_ms = (time.perf_counter() - t_host) * 1e3
+        g1.record(stream)
+        torch.cuda.synchronize()
+        spin_ms = gs.elapsed_time(g0)
+        q_ms = g0.elapsed_time(g1) / reps
+        assert lm.check_states() == 0
         graph = {"workload": f"{R} calls of B={Bb} on 8 streams, one HIP graph replay",
                  "bound": "hbm", "achieved": hbm_bytes / (g_ms * 1e-3) / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                  "frac": hbm_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, "bytes_per_replay": hbm_bytes,
-                 "ms": g_ms, "scores_per_s": B * V / (g_ms * 1e-3)}
-        log(f"advance as {R} graph-captured B={Bb} calls on 8 streams: {g_ms:.3f} ms per replay, "
-            f"{graph['scores_per_s']:.3g} scores/s")
+                 "ms": g_ms, "scores_per_s": B * V / (g_ms * 1e-3),
+                 "host_ms_per_replay_call": host_ms,
+                 "ms_queued": q_ms if enqueue_ms < spin_ms else None,
+                 "frac_queued": (hbm_bytes / (q_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS) if enqueue_ms < spin_ms else None,
+                 "method": "20 replays back to back between HIP events (ms, frac); host_ms_per_replay_call: "
+                           "host time of one replay call in that loop; ms_queued / frac_queued: the 20 "
+                           "replays enqueued while the GPU spins, then timed on the GPU alone"}
+        log(f"advance as {R} graph-captured B={Bb} calls on 8 streams: {g_ms:.3f} ms per replay "
+            f"(host {host_ms:.3f} ms per replay call), {graph['scores_per_s']:.3g} scores/s; "
+            f"queued ahead: {q_ms:.3f} ms per replay (enqueue {enqueue_ms:.1f} ms, spin {spin_ms:.1f} ms)")
         del g_adv
 
     if args.advance_only:

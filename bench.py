@@ -14,8 +14,9 @@ second over the timed steps.  The same run also reports:
   counter summary when it was taken on the current kernel source, else null;
 * latency of a single 512-hypothesis call (median of 100, the calls enqueued
   ahead of the GPU so that the events bracket device time; also the same
-  with the GPU waiting for each call's submission), with its algorithmic
-  bytes as a fraction of the HBM roofline (roofline_b512_single);
+  with the GPU waiting for each call's submission, and the per-call time of
+  100 calls back to back), with its algorithmic bytes as a fraction of the
+  HBM roofline (roofline_b512_single);
 * the same work as 128 separate 512-hypothesis calls on 8 streams, captured in
   one HIP graph, likewise against the roofline (roofline_b512_graph), with
   the host time of each replay call and the GPU's own time per replay when
@@ -178,15 +179,29 @@ def main():
 
     lat_host_us = single_calls(False)
     lat_us = single_calls(True)
-    log(f"single B={Bb} call: median {lat_us:.1f} us of device time ({lat_host_us:.1f} us paced by the host)")
+    # the same 100 calls enqueued back to back with no events between them,
+    # timed as a whole: the per-call cost of a stream of dependent-free calls
+    views = [(states[sl], scores[sl], nxt[sl]) for sl in
+             (slice((r % R) * Bb, (r % R + 1) * Bb) for r in range(100))]
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(int(8e6))
+    b0.record(stream)
+    for st_r, sc_r, nx_r in views:
+        lm.advance(st_r, sc_r, nx_r)
+    b1.record(stream)
+    torch.cuda.synchronize()
+    b2b_us = b0.elapsed_time(b1) * 1e3 / len(views)
+    log(f"single B={Bb} call: median {lat_us:.1f} us of device time ({lat_host_us:.1f} us paced by the host); "
+        f"{b2b_us:.1f} us per call back to back")
     # algorithmic bytes of one 512-hypothesis call: the mean over the slices the 100 calls cycle through
     call_bytes = float(np.mean([lm.query_bytes(states_np[(r % R) * Bb:(r % R + 1) * Bb])[0] for r in range(100)]))
     single = {"bound": "hbm", "achieved": call_bytes / (lat_us * 1e-6) / 1e9, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
               "frac": call_bytes / (lat_us * 1e-6) / 1e9 / PEAK_HBM_GBPS, "bytes_per_call": call_bytes,
-              "us_per_call": lat_us, "us_per_call_host_paced": lat_host_us,
+              "us_per_call": lat_us, "us_per_call_host_paced": lat_host_us, "us_per_call_back_to_back": b2b_us,
               "workload": f"one advance call of B={Bb} uniform states (median of 100, HIP events around each "
                           f"call, enqueued ahead of the GPU; us_per_call_host_paced: the GPU idle until each "
-                          f"call is submitted)"}
+                          f"call is submitted; us_per_call_back_to_back: 100 calls enqueued ahead with no "
+                          f"events between them, timed as a whole)"}
 
     # ---- sustained: one launch over all R batches per step
     for _ in range(args.warmup):

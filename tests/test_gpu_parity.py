@@ -794,11 +794,12 @@ def test_sync_check(dev):
 
 @pytest.mark.parametrize("k", [6, 8, 64, 100, 128, 256])
 def test_fused_topk_large_k(dev, k):
-    """The threshold selection (k >= 6): rows of full ties, -inf rows, rows with
-    fewer finite tokens than k, rows whose fused values are coarsely quantised
-    so that many tokens tie across lanes and stripes, and ordinary rows.  k =
-    64 and 128 are the largest k whose search starts from the smallest lane
-    maximum and lane second-maximum; above 128 it starts from no lower bound."""
+    """The threshold selection (every k at V <= 1024) at larger k: rows of full
+    ties, -inf rows, rows with fewer finite tokens than k, rows whose fused
+    values are coarsely quantised so that many tokens tie across lanes and
+    stripes, and ordinary rows.  k = 64 and 128 are the largest k whose search
+    starts from the smallest lane maximum and lane second-maximum; above 128 it
+    starts from no lower bound."""
     m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     B = 24

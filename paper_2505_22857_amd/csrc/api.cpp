@@ -64,11 +64,13 @@ ngpu::DevTrie dev_view(const ngpu_lm *lm) {
     t.top_begin = int32_t(h.top_arc_begin);
     t.to_delta = h.arc_to_delta;
     t.final_w = h.has_final ? reinterpret_cast<const float *>(base + h.off_final) : nullptr;
+    t.dense_c = h.off_dense_c ? reinterpret_cast<const float *>(base + h.off_dense_c) : nullptr;
+    t.dense_base = h.off_dense_c ? reinterpret_cast<const int32_t *>(base + h.off_dense_base) : nullptr;
+    t.compact_rank = h.compact_rank;
     t.status = reinterpret_cast<int32_t *>(const_cast<unsigned char *>(base) + h.off_status);
     t.num_states = int32_t(lm->S);
     t.vocab_size = lm->V;
     t.max_order = lm->N;
-    t.pad = 0;
     for (int k = 0; k <= NGPU_LM_MAX_ORDER; ++k) t.first[k] = h.first[k];
     for (int k = 0; k < NGPU_LM_MAX_ORDER; ++k) t.off_order[k] = h.off_order[k];
     return t;

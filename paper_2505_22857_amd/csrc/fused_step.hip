@@ -155,6 +155,81 @@ struct RegAsr {
     }
 };
 
+// One wavefront's copy of a compact dense row (DevTrie::dense_c), for the
+// whole decode with rows in registers (W = 1): lane l keeps tokens 64 i + l,
+// loaded like the ASR row (tokens past V read as 0 and are never used).
+template <bool FULL>
+struct CompactRow {
+    float c[kRegTokens / kWave];
+
+    __device__ __forceinline__ void load(const float *row, int V, int lane) {
+        const __amdgpu_buffer_rsrc_t r =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(row), short(0), V * int(sizeof(float)), kBufferConfig);
+#pragma unroll
+        for (int i = 0; i < kRegTokens / kWave; ++i)
+            c[i] = __builtin_bit_cast(float,
+                                      __builtin_amdgcn_raw_buffer_load_b32(r, (kWave * i + lane) * int(sizeof(float)), 0, 0));
+    }
+
+    // Per-lane argmax of fmaf(lambda, lm[v], asr[v]): lm[v] from the LDS row
+    // where a sparse level wrote it (kFinal in ln), else from this row: its
+    // weight (the stored magnitude with the sign bit set) plus acc0 where the
+    // sign bit marks a backed-off entry, acc1 otherwise.
+    __device__ __forceinline__ void fused(const ChainHead &h, const float *ls, const int *ln,
+                                          const RegAsr<1, FULL> &asr, float lambda, int V, int lane, float &bx,
+                                          int &bi) const {
+#pragma unroll
+        for (int i = 0; i < kRegTokens / kWave; ++i) {
+            const int b0 = kWave * i;
+            if (!FULL && b0 >= V) continue;   // uniform; the slots read below lie inside the padded row
+            const int v = b0 + lane;
+            // (both words read unconditionally: a read inside the select
+            // becomes a branch with its own wait, per token)
+            const int n = ln[v];
+            const float x = ls[v];
+            const unsigned cb = __float_as_uint(c[i]);
+            const float dense = ((cb >> 31) ? h.acc0 : h.acc1) + __uint_as_float(cb | 0x80000000u);
+            const float lm = (n & kFinal) ? x : dense;
+            const float f = __builtin_fmaf(lambda, lm, asr.a[i]);
+            if (FULL || b0 + kWave <= V || v < V) take_max(f, v, bx, bi);
+        }
+    }
+
+    // Next state of token w (uniform, w < V): the sparse level's where one
+    // wrote the slot; else, for an own entry of the row when the image
+    // numbers them by rank (orders >= 3), the row's first own-bigram state
+    // (base) plus the number of own entries below w (one ballot per 64
+    // tokens); else the unigram state first[1] + w.
+    __device__ __forceinline__ int next_state(const DevTrie &t, const int *ln, int base, int w, int V,
+                                              int lane) const {
+        const int n = ln[w];
+        if (n & kFinal) return n & kStateMask;
+        const int j = w >> 6, b = w & (kWave - 1);
+        int rank = 0;
+        bool own = false;
+#pragma unroll
+        for (int i = 0; i < kRegTokens / kWave; ++i) {
+            if (i > j) continue;   // uniform
+            const bool mine = (FULL || kWave * i + lane < V) && !(__float_as_uint(c[i]) >> 31);
+            const unsigned long long m = __ballot(mine);
+            if (i < j) {
+                rank += __builtin_popcountll(m);
+            } else {
+                rank += __builtin_popcountll(m & ((1ull << b) - 1ull));
+                own = (m >> b) & 1ull;
+            }
+        }
+        return own && t.compact_rank ? base + rank : t.first[1] + w;
+    }
+};
+
+// Clears the kFinal marks of the LDS next-state row (lds_row(V) words) before
+// the sparse levels write theirs: with compact rows no dense copy overwrites it.
+__device__ __forceinline__ void clear_marks(int *ln, int V, int lane) {
+    const i32x4 z = {0, 0, 0, 0};
+    for (int c = 4 * lane; c < lds_row(V); c += 4 * kWave) *reinterpret_cast<i32x4 *>(ln + c) = z;
+}
+
 struct NoHook {
     __device__ __forceinline__ void operator()() const {}
 };
@@ -296,6 +371,49 @@ __device__ __forceinline__ int greedy_step(const DevTrie &t, const Index &ci, co
     return w;
 }
 
+// The same step for the whole decode with rows in registers and compact
+// dense rows (W = 1): the walk applies the sparse levels only, over cleared
+// marks, and the dense row arrives in registers; the winner's next state
+// follows from the compact row's rules.  Same selection as greedy_step.
+template <int MODE, bool FULL, class AfterRecord>
+__device__ __forceinline__ int greedy_step_compact(const DevTrie &t, const ChainIndex &ci,
+                                                   const RegAsr<1, FULL> &asr, float rowV, float lambda, int &s,
+                                                   int pv, float *ls, int *ln, Exchange *xc, int &xi, int lane,
+                                                   AfterRecord after_record) {
+    const int V = t.vocab_size;
+    const float fin = MODE == kAed ? t.final_w[s] : 0.0f;
+    int nlev;
+    const int4 rec = fetch_record(t, ci, s, lane, nlev);
+    after_record();
+    if (MODE == kCtc || MODE == kTransducer) {
+        float bx = -__builtin_inff(), av;
+        int bi = kNone, unused;
+        asr.argmax(V, 0, lane, bx, bi);
+        int a = group_argmax<1>(bx, bi, 0, av, unused, xc, xi, 0, lane);
+        if (a == kNone) a = 0;
+        if (rowV > av) a = V;
+        if (a == V || (MODE == kCtc && a == pv)) return a;
+    }
+    const ChainHead h = head_of(rec);
+    clear_marks(ln, V, lane);
+    CompactRow<FULL> row;
+    row.load(t.dense_c + size_t(h.dense_row) * size_t(V), V, lane);
+    const int base = t.dense_base[h.dense_row];
+    walk_record<1, false, true>(t, rec, nlev, ls, ln, lane);
+    if (MODE == kCtc && pv >= 0 && pv < V && lane == 0) {
+        ls[pv] = __builtin_nanf("");
+        ln[pv] = kFinal;
+    }
+    float bx = -__builtin_inff(), wv;
+    int bi = kNone, unused;
+    row.fused(h, ls, ln, asr, lambda, V, lane, bx, bi);
+    int w = group_argmax<1>(bx, bi, 0, wv, unused, xc, xi, 0, lane);
+    if (MODE == kAed && __builtin_fmaf(lambda, fin, rowV) > wv) return V;
+    if (w == kNone) w = (MODE == kCtc && pv == 0) ? 1 : 0;   // every candidate at -inf: the first one
+    s = row.next_state(t, ln, base, w, V, lane);
+    return w;
+}
+
 // LDS of one hypothesis: the walked row (ls, ln), nrows ASR rows, the exchange area.
 __host__ __device__ inline size_t hyp_lds_bytes(int V, int nrows) {
     return (2 * size_t(lds_row(V)) + size_t(nrows) * size_t(asr_row_words(V))) * sizeof(float) + sizeof(Exchange);
@@ -356,7 +474,7 @@ __global__ __launch_bounds__(W * kWave) void fused_step_kernel(DevTrie t, const 
 // asr[b * stride_b + t * stride_t + class]; one utterance per workgroup of W
 // wavefronts.  NB: ASR row buffers in LDS (1 or 2), or 0 for rows held in
 // registers (V <= kRegTokens; FULL: V = kRegTokens).
-template <int MODE, int W, int NB, bool FULL = false, bool SPLIT = false>
+template <int MODE, int W, int NB, bool FULL = false, bool SPLIT = false, bool COMPACT = false>
 __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, const float *__restrict__ asr, int64_t B,
                                                                   int64_t T, int64_t stride_b, int64_t stride_t,
                                                                   const int32_t *__restrict__ lengths, float lambda,
@@ -427,8 +545,14 @@ __global__ __launch_bounds__(W * kWave) void fused_decode_kernel(DevTrie t, cons
             RegAsr<W, FULL> nxt_r;
             const float *src = more ? pf : row;
             auto load_next = [&]() { nxt_r.load(src, V, wave, lane); };
-            label = greedy_step<MODE, W, false, RegAsr<W, FULL>, decltype(load_next), SPLIT>(
-                t, ci, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr, nullptr, 0, load_next);
+            if constexpr (COMPACT) {
+                static_assert(W == 1, "compact dense rows serve one wavefront per utterance");
+                label = greedy_step_compact<MODE, FULL>(t, ci, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, lane,
+                                                        load_next);
+            } else {
+                label = greedy_step<MODE, W, false, RegAsr<W, FULL>, decltype(load_next), SPLIT>(
+                    t, ci, cur_r, rowV, lambda, s, pv, ls, ln, xc, xi, wave, lane, nullptr, nullptr, 0, load_next);
+            }
             cur_r = nxt_r;
         } else {
             float *cur = abuf + (kRowBufs == 2 ? (f & 1) * rowp : 0);
@@ -905,6 +1029,14 @@ static hipError_t launch_decode_w(const DevTrie &t, const float *asr, int64_t B,
         if (stripe_split<W>(t)) {
             hipLaunchKernelGGL((fused_decode_kernel<MODE, W, NB, FULL, true>), dim3(unsigned(B)), dim3(W * kWave),
                                hyp_lds_bytes(t.vocab_size, NB), stream, t, asr, B, T, sb, st, lengths, lambda, states,
+                               prev, labels, label_states);
+            return hipGetLastError();
+        }
+    }
+    if constexpr (W == 1 && NB == 0) {
+        if (t.dense_c) {
+            hipLaunchKernelGGL((fused_decode_kernel<MODE, 1, 0, FULL, false, true>), dim3(unsigned(B)), dim3(kWave),
+                               hyp_lds_bytes(t.vocab_size, 0), stream, t, asr, B, T, sb, st, lengths, lambda, states,
                                prev, labels, label_states);
             return hipGetLastError();
         }

@@ -32,6 +32,19 @@
 //   final    float [S]   with </s> in the model: each state's end-of-sentence
 //                        weight, folded through its backoff chain at build
 //                        time (Section 2.3, AED)
+//   dense_c    float [R * V]  the dense rows again in 4 bytes per token, for
+//   dense_base int32 [R]      the whole-decode kernel that holds rows in
+//            registers, which needs a token's next state only for the frame's
+//            winner: dense_c is the weight's magnitude, its sign bit set where
+//            the entry backed off to the empty context (DENSE_BACKOFF), so
+//            weight = dense_c with the sign bit set.  A backed-off token v (and
+//            every token of row 0) leads to the unigram state first[1] + v; an
+//            own bigram of row u leads to dense_base[u] + the number of own
+//            bigrams of row u below it when compact_rank is set (orders >= 3:
+//            bigrams are states, numbered in the row's token order), else to
+//            first[1] + v.  Present (off_dense_c != 0) only when V <= 1024,
+//            every dense weight has its sign bit set and these rules give
+//            dense_to exactly for every entry, which the builder checks.
 #pragma once
 
 #include <cstddef>
@@ -43,7 +56,7 @@
 
 namespace ngpu {
 
-constexpr uint32_t kImageMagic = 0x344d4c4e;  // "NLM4"
+constexpr uint32_t kImageMagic = 0x354d4c4e;  // "NLM5"
 constexpr size_t kAlign = 256;
 constexpr int32_t kDenseBackoff = int32_t(0x80000000u);  // flag bit in dense_to
 constexpr int kGroups = 8;                                // dense-row groups (one per XCD)
@@ -65,9 +78,11 @@ struct ImageHeader {
     uint64_t off_top_arcs;                      // the order-N arcs
     int64_t top_arc_begin;                      // first arc of order N (A3 when there is none)
     int32_t arc_to_delta;                       // next state of arc a of order < N: a + arc_to_delta
-    int32_t pad;
+    int32_t compact_rank;                       // dense_c: own bigrams numbered by their rank in the row
+    uint64_t off_dense_c;                       // compact dense rows (0 when the model does not qualify)
+    uint64_t off_dense_base;                    // int32[R]: first own-bigram state of each dense row
 };
-static_assert(sizeof(ImageHeader) == 248, "the header layout is part of the image format");
+static_assert(sizeof(ImageHeader) == 264, "the header layout is part of the image format");
 
 struct ChainHead {
     int32_t dense_row;
@@ -112,12 +127,14 @@ struct DevTrie {
     const TopArc *top_arcs;   // arcs top_begin .. A3 - 1, at a - top_begin
     const float *final_w;   // nullptr without </s>
     int32_t *status;
+    const float *dense_c;         // nullptr when the model has no compact dense rows
+    const int32_t *dense_base;
     int32_t num_states;
     int32_t vocab_size;
     int32_t max_order;
     int32_t top_begin;      // first arc of the highest order
     int32_t to_delta;       // next state of an arc below top_begin: its index + to_delta
-    int32_t pad;
+    int32_t compact_rank;
     int32_t first[NGPU_LM_MAX_ORDER + 1];
     uint64_t off_order[NGPU_LM_MAX_ORDER];
 };

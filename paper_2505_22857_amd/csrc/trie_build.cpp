@@ -371,6 +371,18 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
     h.has_final = special ? 1 : 0;
     h.off_final = special ? off : 0;
     if (special) off = align_up(off + size_t(S) * 4);
+    // compact dense rows (for the whole decode with rows in registers): room
+    // is made when the vocabulary allows them, and given back below if the
+    // model does not qualify
+    const size_t off_without_compact = off;
+    const bool try_compact = V >= 2 && V <= 1024 && N >= 2;
+    h.compact_rank = N > 2 ? 1 : 0;
+    if (try_compact) {
+        h.off_dense_c = off;
+        off = align_up(off + size_t(R) * size_t(V) * 4);
+        h.off_dense_base = off;
+        off = align_up(off + size_t(R) * 4);
+    }
     h.start_state = 0;
     if (special && N > 1) h.start_state = int32_t(first[1] + find_rank(lv[1].key, u128(uint32_t(bos))));
     h.total_bytes = off;
@@ -417,6 +429,44 @@ int build_trie(const ngpu_ngram_list *list, int32_t V, float unk, uint32_t flags
             rt[v] = N > 2 ? int32_t(first[2] + a) : int32_t(first[1] + L2.suffix[a]);
         }
     }
+    // compact dense rows: the weight's magnitude with the sign bit as the
+    // backoff flag; kept only if every weight's sign bit is set and the
+    // next-state rules reproduce dense_to for every entry
+    if (try_compact) {
+        float *dc = reinterpret_cast<float *>(img.data() + h.off_dense_c);
+        int32_t *db = reinterpret_cast<int32_t *>(img.data() + h.off_dense_base);
+        bool ok = true;
+        for (int64_t u = 0; u < R && ok; ++u) {
+            const float *rw = dense_w + size_t(u) * size_t(V);
+            const int32_t *rt = dense_to + size_t(u) * size_t(V);
+            float *rc = dc + size_t(u) * size_t(V);
+            int32_t base = u == 0 ? int32_t(first[1]) : -1, rank = 0;
+            for (int32_t v = 0; v < V && ok; ++v) {
+                uint32_t wb;
+                std::memcpy(&wb, &rw[v], 4);
+                const bool backoff = (rt[v] & kDenseBackoff) != 0;
+                const int32_t to = rt[v] & ~kDenseBackoff;
+                const uint32_t cb = backoff ? wb : (wb & 0x7fffffffu);
+                std::memcpy(&rc[v], &cb, 4);
+                int64_t want = first[1] + v;
+                if (!backoff && h.compact_rank) {   // own entry (every entry of row 0)
+                    if (base < 0) base = to;
+                    want = int64_t(base) + rank++;
+                }
+                ok = (wb & 0x80000000u) && to == want;
+            }
+            db[u] = base < 0 ? 0 : base;
+        }
+        if (!ok) {
+            h.off_dense_c = 0;
+            h.off_dense_base = 0;
+            off = off_without_compact;
+            h.total_bytes = off;
+            img.resize(off);
+            std::memcpy(img.data(), &h, sizeof h);
+        }
+    }
+
     // sparse arcs of orders 3..N: token and weight; the next state is the
     // arc's own n-gram (k < N: first[k] + p = a + first[3], as arc_base[k] -
     // arc3 and first[k] - first[3] both count the orders 3 .. k-1) or, for

@@ -474,6 +474,40 @@ def test_decode_launch_row_placements(dev, V, B):
         assert np.array_equal(gs, os_)
 
 
+@pytest.mark.parametrize("which", ["bigram", "zero_weight", "trigram"])
+def test_decode_register_rows_dense_forms(dev, which):
+    """Register-row decodes (2400 utterances at V = 1000) through both dense-row
+    forms: a trigram model, whose 4-byte dense rows lead own bigrams to the
+    row's base plus their rank; a bigram model, whose own entries lead to
+    unigram states; and a trigram model with one bigram weight at +0.0 (sign
+    bit clear), which gets no 4-byte rows, so the 8-byte rows serve it."""
+    import struct
+    V, B, T = 1000, 2400, 10
+    if which == "bigram":
+        m = generate_model(V, [V, 30000], 1.0, seed=11)
+    else:
+        m = generate_model(V, [V, 20000, 15000], 1.0, seed=12)
+    order, tokens, W, Bo = m.to_list()
+    if which == "zero_weight":
+        W = W.copy()
+        W[np.nonzero(order == 2)[0][5]] = 0.0
+    lm = ng.NgpuLM(V, m.max_order, order, tokens, W, Bo, m.unk_logprob).upload(dev)
+    o = Oracle(V, m.max_order, order, tokens, W, Bo, m.unk_logprob)
+    hdr = struct.unpack_from("<IiiiqqQQQQQQ11i4x10QQiiQqiiQQ", lm.host_image()[:264].tobytes())
+    assert (hdr[40] != 0) == (which != "zero_weight")
+    starts = uniform_states(m, B, seed=13)
+    asr = asr_logprobs((B, T, V + 1), seed=14, blank_boost=0.5)
+    for mode in (MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER):
+        a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+        case(f"decode launch register rows {which} mode={mode}")
+        gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
+        assert lm.check_states() == 0
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
+        bad = np.argwhere(gl != ol)
+        assert len(bad) == 0, f"labels differ first at {bad[0]}"
+        assert np.array_equal(gs, os_)
+
+
 @pytest.mark.parametrize("V,B", [(1024, 32), (1024, 600), (1024, 2400), (1000, 2400)])
 def test_decode_launch_time_major_view(dev, V, B):
     """The whole decode reads a time-major [T, B, C] buffer through a permuted

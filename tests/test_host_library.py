@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(lib):
     assert sorted(ng.EXPORTED) == decl
 
 
-HDR_FMT = "<IiiiqqQQQQQQ11i4x10QQiiQqii"
+HDR_FMT = "<IiiiqqQQQQQQ11i4x10QQiiQqiiQQ"
 
 
 def parse_image(img):
@@ -52,8 +52,9 @@ def parse_image(img):
     first = list(f[12:23])
     off_order = list(f[23:33])
     off_final, start_state, has_final, o_top, top_begin, delta = f[33:39]
-    assert struct.calcsize(HDR_FMT) == 248
-    assert magic == 0x344D4C4E and total == len(img)
+    compact_rank, o_dc, o_db = f[39:42]
+    assert struct.calcsize(HDR_FMT) == 264
+    assert magic == 0x354D4C4E and total == len(img)
     lo = np.frombuffer(raw, np.int32, 2 * top_begin, o_arc).reshape(top_begin, 2)    # {token, weight bits}
     hi = np.frombuffer(raw, np.int32, 3 * (A3 - top_begin), o_top).reshape(-1, 3)  # {token, weight bits, next}
     arcs = np.concatenate([lo, hi[:, :2]])
@@ -64,7 +65,63 @@ def parse_image(img):
                 dense_to=np.frombuffer(raw, np.int32, R * V, o_dt).reshape(R, V),
                 tok=arcs[:, 0].copy(), w=arcs[:, 1].copy().view(np.float32), to=to,
                 start_state=start_state,
-                final=np.frombuffer(raw, np.float32, S, off_final) if has_final else None)
+                final=np.frombuffer(raw, np.float32, S, off_final) if has_final else None,
+                compact_rank=compact_rank,
+                dense_c=np.frombuffer(raw, np.uint32, R * V, o_dc).reshape(R, V) if o_dc else None,
+                dense_base=np.frombuffer(raw, np.int32, R, o_db) if o_dc else None)
+
+
+@pytest.mark.parametrize("which", ["trigram_v128", "fourgram_200k", "n2", "n10", "bos_eos", "tiny-unk", "n1",
+                                   "positive"])
+def test_compact_dense_rows(which):
+    """The 4-byte dense rows of the register decode: present exactly when V <= 1024,
+    every dense weight is negative (sign bit set) and every unigram is listed;
+    then the weight is the stored magnitude with the sign bit set, the sign bit
+    marks the backed-off entries, and a token's next state is first[1] + v for
+    backed-off entries (and row 0), else (orders >= 3) the row's base plus the
+    token's rank among the row's own entries, as the 8-byte rows hold it."""
+    expect = True
+    if which in ("trigram_v128", "fourgram_200k"):
+        m = make_model(which)
+    elif which == "n2":
+        m = generate_model(40, [40, 400], 1.0, seed=1)
+    elif which == "n10":
+        m = generate_model(16, [16, 120, 200, 200, 180, 160, 140, 120, 100, 80], 1.0, seed=3)
+    elif which == "bos_eos":
+        m = generate_model(24, [24, 180, 240, 200], 1.0, seed=3, bos_eos=True)
+    elif which == "tiny-unk":
+        m, expect = tiny_model(9, 3, seed=21, n_unigrams=6), False
+    elif which == "n1":
+        m, expect = generate_model(40, [40], 1.0, seed=1), False
+    else:
+        m, expect = generate_model(40, [40, 400], 1.0, seed=1), False
+    if which == "positive":   # one weight at +0.0: its sign bit is clear
+        order, tokens, W, B = m.to_list()
+        W = W.copy()
+        W[np.nonzero(order == 2)[0][0]] = 0.0
+        lm = ng.NgpuLM(m.vocab_size, m.max_order, order, tokens, W, B, m.unk_logprob)
+    else:
+        lm = ng.NgpuLM.from_model(m)
+    im = parse_image(lm.host_image())
+    assert (im["dense_c"] is not None) == expect
+    if not expect:
+        return
+    V, f1 = im["V"], im["first"][1]
+    wbits = im["dense_w"].view(np.uint32)
+    c = im["dense_c"]
+    assert np.array_equal(c | np.uint32(0x80000000), wbits)
+    backoff = im["dense_to"] < 0
+    assert not backoff[0].any()
+    assert np.array_equal(c >> 31 == 1, backoff)
+    for u in range(im["R"]):
+        own = ~backoff[u]
+        nxt = np.full(V, -1, np.int64)
+        nxt[~own] = f1 + np.nonzero(~own)[0]
+        if im["compact_rank"] and u > 0:
+            nxt[own] = im["dense_base"][u] + np.arange(own.sum())
+        else:
+            nxt[own] = f1 + np.nonzero(own)[0]
+        assert np.array_equal(nxt, im["dense_to"][u] & 0x7FFFFFFF), (which, u)
 
 
 def chain_of(im, s):

@@ -1082,13 +1082,16 @@ static hipError_t launch_decode_mode(const DevTrie &t, const float *asr, int64_t
     if (waves_per_hyp(B) == 4)
         return launch_decode_w<MODE, 4, 2>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
                                            stream);
-    // Measured on the 20M 6-gram, CTC, 200 frames: while every utterance is
-    // resident with two LDS row buffers (2304 utterances on 256 CUs at
-    // V = 1024), those are 2-4 % faster than rows in registers; beyond that
-    // the register rows (up to 16 utterances per CU) are 27 % faster at 4096
-    // utterances and 18 % at 8192, and one LDS buffer (13 per CU) still beats
-    // two by 8-14 %.
-    if (B <= resident_double_buffered(t))
+    // Measured on the 20M 6-gram, CTC, 200 frames: with compact dense rows
+    // the register rows are the fastest at every size (0.556 / 0.571 / 0.611
+    // / 0.625 / 0.654 ms against 0.624 / 0.638 / 0.696 / 0.705 / 0.789 ms for
+    // two LDS row buffers at 600 / 1024 / 1536 / 2048 / 2304 utterances).
+    // Without them: while every utterance is resident with two LDS row
+    // buffers (2304 utterances on 256 CUs at V = 1024), those are 2-4 % faster
+    // than rows in registers; beyond that the register rows (up to 16
+    // utterances per CU) are 27 % faster at 4096 utterances and 18 % at 8192,
+    // and one LDS buffer (13 per CU) still beats two by 8-14 %.
+    if (!(t.dense_c && t.vocab_size <= kRegTokens) && B <= resident_double_buffered(t))
         return launch_decode_w<MODE, 1, 2>(t, asr, B, T, sb, st, lengths, lambda, states, prev, labels, label_states,
                                            stream);
     if (t.vocab_size == kRegTokens)

@@ -428,9 +428,8 @@ def test_decode_launch_modes_ragged_lengths(dev, mode):
 def test_fused_larger_batches(dev, B):
     """Batches above 512 hypotheses: the whole decode runs with one wavefront
     per hypothesis instead of four (the per-frame step from 1025 on, so 513
-    covers its four-wavefront path at that size); at 5000 utterances (more
-    than the 256 CUs hold at once with two V = 1024 ASR rows in LDS each) the
-    whole decode keeps the rows in registers."""
+    covers its four-wavefront path at that size), with the ASR rows and the
+    4-byte dense rows in registers (this model has them)."""
     m, lm, o = model_pair("fourgram_200k")
     V = m.vocab_size
     T = 16
@@ -450,12 +449,12 @@ def test_fused_larger_batches(dev, B):
                                  (2048, 1500)])
 def test_decode_launch_row_placements(dev, V, B):
     """The whole decode with one wavefront per utterance keeps the ASR rows in
-    two LDS buffers while every utterance is resident at once with them (on
-    256 CUs with 160 KiB of LDS each: 9984 utterances at V = 40, 2304 at
-    V = 1000 or 1024, 1792 at V = 1025, 1024 at V = 2048); beyond that in
-    registers up to V = 1024 (with and without a last register chunk cut short
-    by V, or with most chunks past V), else in one LDS buffer.
-    The cases cover each placement, and the four fusion modes on the register
+    registers up to V = 1024 when the model has 4-byte dense rows (these
+    models do; with and without a last register chunk cut short by V, or with
+    most chunks past V); above V = 1024 in two LDS buffers while every
+    utterance is resident at once with them (on 256 CUs with 160 KiB of LDS
+    each: 1792 at V = 1025, 1024 at V = 2048), else in one LDS buffer.  The
+    cases cover each placement, and the four fusion modes on the register
     paths."""
     m, lm, o = pair(f"V{V}", lambda: generate_model(V, [V, 20000, 15000], 1.0, seed=V, bos_eos=True))
     T = 10
@@ -512,9 +511,9 @@ def test_decode_register_rows_dense_forms(dev, which):
 def test_decode_launch_time_major_view(dev, V, B):
     """The whole decode reads a time-major [T, B, C] buffer through a permuted
     [B, T, C] view (utterance stride C, frame stride B * C) whose rows carry
-    padding past the classes: every row placement (four wavefronts, two LDS
-    buffers, registers with and without a short last chunk) must read only
-    the V (+ 1) classes of its own row."""
+    padding past the classes: four wavefronts with LDS rows, and registers
+    with and without a short last chunk, must read only the V (+ 1) classes
+    of its own row."""
     if V == 1024:
         m, lm, o = model_pair("fourgram_200k")
     else:

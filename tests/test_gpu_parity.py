@@ -405,6 +405,27 @@ def test_decode_launch_ctc_256x1000(dev):
     print(f"  CTC 256x1000 one launch: {gl.size} decisions identical", flush=True)
 
 
+def test_decode_launch_20m_register_rows(dev):
+    """The 20M 6-gram decoded with one wavefront per utterance and the ASR and
+    4-byte dense rows in registers (4096 utterances x 24 frames, the shape of
+    the benchmark's large decode), from uniformly drawn states (deep chains)
+    and from the empty context, against the oracle."""
+    m, lm, o = model_pair("sixgram_20m")
+    V, B, T = m.vocab_size, 4096, 24
+    asr = asr_logprobs((B, T, V + 1), seed=91, blank_boost=4.0)
+    starts = uniform_states(m, B, seed=92)
+    starts[::2] = 0
+    for mode in (MODE_CTC, MODE_PLAIN):
+        a = asr if mode != MODE_PLAIN else np.ascontiguousarray(asr[:, :, :V])
+        case(f"decode launch 20M register rows B={B} T={T} mode={mode}")
+        gl, gs, _, _ = gpu_decode_launch(lm, a, mode, 0.5, starts, dev)
+        assert lm.check_states() == 0
+        ol, os_ = o.decode(a, mode, 0.5, starts, nthreads=NTHREADS)
+        bad = np.argwhere(gl != ol)
+        assert len(bad) == 0, f"labels differ first at {bad[0]}"
+        assert np.array_equal(gs, os_)
+
+
 @pytest.mark.parametrize("mode", [MODE_PLAIN, MODE_CTC, MODE_TRANSDUCER])
 def test_decode_launch_modes_ragged_lengths(dev, mode):
     m, lm, o = model_pair("fourgram_200k")
